@@ -1,0 +1,282 @@
+"""Seeded synthetic workloads: trees in breadth-first node-array form and fp32 feature matrices.
+
+This module only draws random numbers and lays them out; it evaluates nothing.  Both the
+GPU path and the CPU oracle consume what it produces, so it must stay free of the
+method's arithmetic (no comparisons of features against thresholds, no walks).
+
+Node arrays follow the breadth-first encoding of Procedure 1 (Section 3.1): node ``i``
+stores ``(feature, threshold, left, cls)``; the right child is ``left + 1``; ``cls = -1``
+marks an internal (decision) node.  Features are 0-based (the paper counts from 1).
+
+The five configurations are the evaluation workloads of this implementation:
+
+    C1  N=65,536     F=8   U[0,1)  complete depth-4 tree,  4 classes
+    C2  N=262,144    F=16  U[0,1)  complete depth-8 tree,  8 classes (512x512 image)
+    C3  N=2,073,600  F=32  N(0,1)  random tree, p_split=0.85, depth<=16, <=1,023 internal, 16 classes
+    C4  N=16,777,216 F=64  U[0,1)  complete depth-12 tree, 32 classes
+    C5  N=4,194,304  F=32  U[0,1)  forest of 32 complete depth-10 trees, 8 classes
+
+C1 and C2 stand in for the paper's image-segmentation workload (Section 4.1), whose
+records and trained tree are not available: they keep its shape (a 256x256 or 512x512
+image of independent records) with synthetic i.i.d. features.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import List, Optional
+
+import numpy as np
+
+NODE_DTYPE = np.dtype(
+    [("feature", "<i4"), ("threshold", "<f4"), ("left", "<i4"), ("cls", "<i4")], align=False
+)
+assert NODE_DTYPE.itemsize == 16
+
+SEED_BASE = 137300
+
+
+@dataclasses.dataclass
+class TreeWorkload:
+    name: str
+    nodes: np.ndarray          # NODE_DTYPE, one tree (or all trees concatenated for a forest)
+    n_features: int
+    n_classes: int
+    n_samples: int
+    feature_dist: str          # "uniform" or "normal"
+    seed: int
+    tree_offsets: Optional[np.ndarray] = None   # forest only: int32[n_trees + 1]
+
+    @property
+    def is_forest(self) -> bool:
+        return self.tree_offsets is not None
+
+    def features(self, n: Optional[int] = None, start: int = 0) -> np.ndarray:
+        """Row-major fp32 matrix of ``n`` rows (default: all), rows ``start .. start+n``.
+
+        Rows are generated in fixed blocks so that any slice is identical to the same rows
+        of the full matrix.
+        """
+        n = self.n_samples - start if n is None else n
+        return feature_rows(self.seed, self.n_features, self.feature_dist, start, n)
+
+
+# ----------------------------------------------------------------------------------------
+# random streams
+
+def _streams(seed: int):
+    ss = np.random.SeedSequence(seed)
+    tree_ss, feat_ss = ss.spawn(2)
+    return tree_ss, feat_ss
+
+
+def uniform_f32(rng: np.random.Generator, shape) -> np.ndarray:
+    """U[0,1) on the 24-bit grid k * 2**-24 (numpy's float32 generator)."""
+    return rng.random(shape, dtype=np.float32)
+
+
+def normal_f32(rng: np.random.Generator, shape) -> np.ndarray:
+    return rng.standard_normal(shape, dtype=np.float32)
+
+
+_BLOCK_ROWS = 1 << 16
+
+
+def feature_rows(seed: int, n_features: int, dist: str, start: int, n: int) -> np.ndarray:
+    """Rows ``start .. start+n`` of the feature matrix of a workload.
+
+    The matrix is produced in blocks of 65,536 rows, each from its own child seed, so a
+    slice can be produced without generating the rows before it.
+    """
+    if n < 0 or start < 0:
+        raise ValueError("negative row range")
+    out = np.empty((n, n_features), dtype=np.float32)
+    if n == 0:
+        return out
+    _, feat_ss = _streams(seed)
+    b0 = start // _BLOCK_ROWS
+    b1 = (start + n - 1) // _BLOCK_ROWS
+    for b in range(b0, b1 + 1):
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(
+            entropy=feat_ss.entropy, spawn_key=feat_ss.spawn_key + (b,))))
+        if dist == "uniform":
+            blk = uniform_f32(rng, (_BLOCK_ROWS, n_features))
+        elif dist == "normal":
+            blk = normal_f32(rng, (_BLOCK_ROWS, n_features))
+        else:
+            raise ValueError(dist)
+        lo = max(start, b * _BLOCK_ROWS)
+        hi = min(start + n, (b + 1) * _BLOCK_ROWS)
+        out[lo - start:hi - start] = blk[lo - b * _BLOCK_ROWS:hi - b * _BLOCK_ROWS]
+    return out
+
+
+# ----------------------------------------------------------------------------------------
+# trees
+
+def complete_tree(rng: np.random.Generator, depth: int, n_features: int, n_classes: int,
+                  threshold_dist: str = "uniform") -> np.ndarray:
+    """Complete binary tree of the given depth in breadth-first (heap) order.
+
+    Internal node i has children 2i+1 and 2i+2, which is exactly what Procedure 1 assigns
+    to a complete tree.  Depth counts edges, so there are 2**depth - 1 internal nodes and
+    2**depth leaves.
+    """
+    n_int = (1 << depth) - 1
+    n_leaf = 1 << depth
+    nodes = np.zeros(n_int + n_leaf, dtype=NODE_DTYPE)
+    feats = rng.integers(0, n_features, size=n_int, dtype=np.int32)
+    if threshold_dist == "uniform":
+        thr = uniform_f32(rng, n_int)
+    else:
+        thr = normal_f32(rng, n_int)
+    cls = rng.integers(0, n_classes, size=n_leaf, dtype=np.int32)
+    idx = np.arange(n_int, dtype=np.int32)
+    nodes["feature"][:n_int] = feats
+    nodes["threshold"][:n_int] = thr
+    nodes["left"][:n_int] = 2 * idx + 1
+    nodes["cls"][:n_int] = -1
+    nodes["feature"][n_int:] = 0
+    nodes["threshold"][n_int:] = 0.0
+    nodes["left"][n_int:] = -1
+    nodes["cls"][n_int:] = cls
+    return nodes
+
+
+def grown_tree(rng: np.random.Generator, p_split: float, max_depth: int, max_internal: int,
+               n_features: int, n_classes: int, threshold_dist: str = "normal") -> np.ndarray:
+    """Random full binary tree grown breadth-first.
+
+    Nodes are created in breadth-first order, so creation order is the Procedure 1 index.
+    The root always splits; any other node at depth d splits iff d < max_depth, the
+    internal-node cap is not yet reached, and a uniform draw is below ``p_split``.  Once
+    the cap is reached every remaining frontier node becomes a leaf.  Per node the draws
+    are: split uniform (float64), then feature and threshold (internal) or class (leaf).
+    """
+    feature: List[int] = []
+    threshold: List[float] = []
+    left: List[int] = []
+    cls: List[int] = []
+    depth_of: List[int] = [0]
+    # node 0 exists; queue holds indices awaiting a decision
+    queue = [0]
+    n_created = 1
+    n_internal = 0
+    feature.append(0); threshold.append(0.0); left.append(-1); cls.append(-1)
+    head = 0
+    while head < len(queue):
+        i = queue[head]; head += 1
+        d = depth_of[i]
+        u = rng.random()
+        split = (i == 0 or u < p_split) and d < max_depth and n_internal < max_internal
+        if split:
+            n_internal += 1
+            feature[i] = int(rng.integers(0, n_features))
+            if threshold_dist == "normal":
+                threshold[i] = float(normal_f32(rng, 1)[0])
+            else:
+                threshold[i] = float(uniform_f32(rng, 1)[0])
+            left[i] = n_created
+            cls[i] = -1
+            for _ in range(2):
+                feature.append(0); threshold.append(0.0); left.append(-1); cls.append(-1)
+                depth_of.append(d + 1)
+                queue.append(n_created)
+                n_created += 1
+        else:
+            cls[i] = int(rng.integers(0, n_classes))
+            left[i] = -1
+    nodes = np.zeros(n_created, dtype=NODE_DTYPE)
+    nodes["feature"] = feature
+    nodes["threshold"] = np.asarray(threshold, dtype=np.float32)
+    nodes["left"] = left
+    nodes["cls"] = cls
+    return nodes
+
+
+def random_full_tree(rng: np.random.Generator, n_internal: int, n_features: int,
+                     n_classes: int, threshold_values: Optional[np.ndarray] = None) -> np.ndarray:
+    """Random full binary tree with exactly ``n_internal`` internal nodes (any shape).
+
+    Shapes come from repeatedly splitting a uniformly chosen leaf; the result is then
+    renumbered breadth-first as Procedure 1 does.  ``threshold_values``, if given, is the
+    pool thresholds are drawn from (to force ties and special values in tests).
+    """
+    # build with explicit children first
+    kids = {0: None}
+    leaves = [0]
+    nxt = 1
+    for _ in range(n_internal):
+        k = int(rng.integers(0, len(leaves)))
+        v = leaves.pop(k)
+        kids[v] = (nxt, nxt + 1)
+        kids[nxt] = None
+        kids[nxt + 1] = None
+        leaves += [nxt, nxt + 1]
+        nxt += 2
+    # breadth-first renumbering (Procedure 1)
+    order = []
+    q = [0]
+    h = 0
+    while h < len(q):
+        v = q[h]; h += 1
+        order.append(v)
+        if kids[v] is not None:
+            q += list(kids[v])
+    new_id = {v: i for i, v in enumerate(order)}
+    nodes = np.zeros(len(order), dtype=NODE_DTYPE)
+    for v in order:
+        i = new_id[v]
+        if kids[v] is None:
+            nodes[i] = (0, 0.0, -1, int(rng.integers(0, n_classes)))
+        else:
+            if threshold_values is None:
+                t = float(uniform_f32(rng, 1)[0])
+            else:
+                t = float(threshold_values[int(rng.integers(0, len(threshold_values)))])
+            nodes[i] = (int(rng.integers(0, n_features)), t, new_id[kids[v][0]], -1)
+    return nodes
+
+
+def config(k: int, n_samples: Optional[int] = None) -> TreeWorkload:
+    """Workload C1..C5 (``k`` in 1..5).  ``n_samples`` may shrink the sample count."""
+    seed = SEED_BASE + k
+    tree_ss, _ = _streams(seed)
+    rng = np.random.Generator(np.random.PCG64(tree_ss))
+    if k == 1:
+        w = TreeWorkload("C1", complete_tree(rng, 4, 8, 4), 8, 4, 65_536, "uniform", seed)
+    elif k == 2:
+        w = TreeWorkload("C2", complete_tree(rng, 8, 16, 8), 16, 8, 262_144, "uniform", seed)
+    elif k == 3:
+        s = seed
+        while True:
+            nodes = grown_tree(rng, 0.85, 16, 1023, 32, 16, "normal")
+            if int((nodes["cls"] < 0).sum()) >= 512:
+                break
+            s += 1
+            rng = np.random.Generator(np.random.PCG64(_streams(s)[0]))
+        w = TreeWorkload("C3", nodes, 32, 16, 2_073_600, "normal", seed)
+    elif k == 4:
+        w = TreeWorkload("C4", complete_tree(rng, 12, 64, 32), 64, 32, 16_777_216, "uniform", seed)
+    elif k == 5:
+        trees = []
+        for t_ss in tree_ss.spawn(32):
+            trng = np.random.Generator(np.random.PCG64(t_ss))
+            trees.append(complete_tree(trng, 10, 32, 8))
+        offsets = np.zeros(33, dtype=np.int32)
+        offsets[1:] = np.cumsum([len(t) for t in trees])
+        w = TreeWorkload("C5", np.concatenate(trees), 32, 8, 4_194_304, "uniform", seed,
+                         tree_offsets=offsets)
+    else:
+        raise ValueError("config index must be 1..5")
+    if n_samples is not None:
+        w.n_samples = int(n_samples)
+    return w
+
+
+CONFIG_DESCRIPTIONS = {
+    1: "C1: N=65,536 x F=8 fp32 U[0,1); complete depth-4 tree (15 internal), 4 classes",
+    2: "C2: N=262,144 (512x512) x F=16 fp32 U[0,1); complete depth-8 tree (255 internal), 8 classes",
+    3: "C3: N=2,073,600 (1920x1080) x F=32 fp32 N(0,1); random tree p=0.85, depth<=16, <=1,023 internal, 16 classes",
+    4: "C4: N=16,777,216 x F=64 fp32 U[0,1); complete depth-12 tree (4,095 internal), 32 classes",
+    5: "C5: N=4,194,304 x F=32 fp32 U[0,1); forest of 32 complete depth-10 trees, 8 classes, majority vote",
+}
