@@ -1,0 +1,216 @@
+/*
+ * dtree.h -- C ABI of the MI355X (gfx950) classification-tree evaluator.
+ *
+ * Evaluates a trained full binary classification tree with continuous-attribute tests
+ * over every record of an fp32 feature matrix, following Spencer, "Speculative Parallel
+ * Evaluation of Classification Trees on GPGPU Compute Engines":
+ *   - DT_ALGO_DATA: the data decomposition of Section 3.2 (Procedure 3): one GPU lane
+ *     per record walks the tree without branches.
+ *   - DT_ALGO_SPECULATIVE: the speculative decomposition of Sections 3.3-3.4
+ *     (Procedures 4-5): a group of lanes evaluates every decision node of a block of
+ *     the tree for one record at once, the per-node outcomes are gathered into a
+ *     64-bit wavefront mask, and the reached node is found by walking the mask.  Trees
+ *     deeper than one block are evaluated block after block (the "window" of
+ *     Section 6).
+ *   - Forests (Section 1, trees evaluated one after another and combined): majority
+ *     vote, ties to the smallest class id.
+ *
+ * Decision rule: a record x goes to the LEFT child of node n iff x[feature_n] <
+ * threshold_n, and to the RIGHT child otherwise.  Ties (x == t) and NaN features go
+ * right.  IEEE comparison: -0.0 == +0.0, denormals are not flushed.  The paper states
+ * the complementary form (left iff x <= t); a tree in that form converts exactly by
+ * replacing each threshold t by nextafterf(t, +inf) (for t < +inf).
+ *
+ * Tree layout: the breadth-first array of Procedure 1 (Section 3.1).  Node i stores
+ * its feature, threshold, the index of its LEFT child and a class; the right child is
+ * left + 1.  A decision node has cls == -1 (the paper's "no class").  Procedure 1 emits
+ * exactly this layout; any node order is accepted as long as every child index is
+ * larger than its parent's index, every node but the root has exactly one parent, and
+ * the tree is full (every decision node has two children).
+ *
+ * Threading: handles are immutable after creation; classify calls on the same handle
+ * may run concurrently on different streams.  All calls are noexcept: no C++ exception
+ * crosses the ABI.  The last error message of the calling thread is available from
+ * dt_last_error().
+ */
+#ifndef DTREE_H
+#define DTREE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DT_ABI_VERSION 1
+
+typedef enum {
+    DT_OK = 0,
+    DT_ERR_INVALID_ARG = 1,   /* null pointer, negative size, ld < n_features, bad enum   */
+    DT_ERR_INVALID_TREE = 2,  /* not a full binary tree in the layout above, or a feature
+                                 or class out of range                                     */
+    DT_ERR_UNSUPPORTED = 3,   /* valid input beyond this library's limits (see below)     */
+    DT_ERR_HIP = 4,           /* a HIP runtime call failed                                 */
+    DT_ERR_NO_MEMORY = 5      /* host or device allocation failed                          */
+} dt_status;
+
+typedef enum {
+    DT_ALGO_DATA = 0,         /* one lane per record (Procedure 3)                          */
+    DT_ALGO_SPECULATIVE = 1   /* lanes per decision node, predicate mask walk (Proc. 4-5)  */
+} dt_algo;
+
+typedef enum {
+    DT_OUT_CLASS_U8 = 0,      /* uint8_t label per record; requires n_classes <= 256      */
+    DT_OUT_CLASS_I32 = 1,     /* int32_t label per record                                   */
+    DT_OUT_LEAF_I32 = 2       /* int32_t index (in the node array) of the leaf reached;
+                                 single trees only                                          */
+} dt_output;
+
+/* One node of the breadth-first array (Procedure 1).  16 bytes, no padding. */
+typedef struct {
+    int32_t feature;    /* 0-based attribute index (the paper counts from 1); decision nodes */
+    float threshold;    /* any float, including +-inf and NaN; decision nodes               */
+    int32_t left;       /* index of the left child; right child = left + 1; decision nodes  */
+    int32_t cls;        /* class in [0, n_classes) for a leaf, -1 for a decision node        */
+} dt_node;
+
+typedef struct dt_tree dt_tree;
+typedef struct dt_forest dt_forest;
+
+/*
+ * Evaluation layout options.  Both decompositions cut the tree into blocks ("windows",
+ * Section 6) of at most `depth` levels, each embedded in a complete subtree of 2^depth - 1
+ * slots.  0 selects the library's choice.
+ *   data_window_depth: 1..16.  Default: the depth that makes the tables smallest.
+ *   spec_window_depth: 1..6 (a window has at most 63 decision nodes, one 64-lane
+ *     wavefront).  2^depth lanes evaluate one record, so 64 / 2^depth records share a
+ *     wavefront instruction.  Default: 4 (16 lanes: 15 decision nodes and one idle lane,
+ *     the half-warp record groups of the paper's experiment, Section 4.2), or the tree
+ *     depth if smaller.
+ */
+typedef struct {
+    int32_t data_window_depth;
+    int32_t spec_window_depth;
+} dt_tree_options;
+
+/* Shape of a tree and of its two encodings. */
+typedef struct {
+    int32_t n_nodes, n_internal, n_leaves;
+    int32_t depth;                  /* edges on the longest root-to-leaf path            */
+    int32_t n_features, n_classes;
+    int32_t data_window_depth, data_windows, data_levels;
+    int32_t spec_window_depth, spec_windows, spec_levels;
+    int64_t data_table_bytes, spec_table_bytes;   /* bytes staged in LDS per workgroup  */
+} dt_tree_info;
+
+/* Version of this ABI (DT_ABI_VERSION of the header the library was built from). */
+int32_t dt_abi_version(void);
+
+/* Static description of a status code.  Never NULL. */
+const char *dt_status_string(dt_status s);
+
+/* Detailed message of the calling thread's last failed call ("" if none).  The pointer
+ * stays valid until the thread's next dt_* call. */
+const char *dt_last_error(void);
+
+/*
+ * Validate a tree and describe its encodings.  Host only: touches no GPU.
+ *   nodes      host array of n_nodes records (read only; not retained)
+ *   opt        may be NULL (defaults)
+ *   info       out, may be NULL
+ * Errors: DT_ERR_INVALID_ARG (null nodes, n_nodes < 1, n_features < 1, n_classes < 1,
+ * option out of range), DT_ERR_INVALID_TREE (see the layout rules above),
+ * DT_ERR_UNSUPPORTED (n_nodes > 2^24).
+ */
+dt_status dt_tree_check(const dt_node *nodes, int32_t n_nodes, int32_t n_features,
+                        int32_t n_classes, const dt_tree_options *opt, dt_tree_info *info);
+
+/*
+ * Window encoding used by the GPU kernels, written to caller-owned host buffers.  Host
+ * only.  Window w occupies slots [w*2^d, (w+1)*2^d) of each array (d = window_depth):
+ *   features[], thresholds[]  slot h < 2^d - 1 is heap position h of the window (children
+ *                   2h+1, 2h+2); a slot that holds no decision node has feature 0 and
+ *                   threshold -inf, so it always sends a record right.  Slot 2^d - 1 is
+ *                   padding with the same values.
+ *   exit_class[], exit_leaf[]  entry e is the outcome of leaving the window at bottom
+ *                   position e (heap position 2^d - 1 + e): a value v >= 0 is the window
+ *                   to continue in; v < 0 ends the walk with class (resp. leaf index)
+ *                   -v - 1.  A leaf met above the bottom level is recorded at the exit
+ *                   reached by always going right from it.
+ * Window 0 is rooted at node 0; windows are numbered in breadth-first order of their roots.
+ * Call with capacity_windows = 0 (buffers may be NULL) to learn *n_windows and *levels
+ * (the largest number of windows on a root-to-leaf path).  Errors as dt_tree_check, plus
+ * DT_ERR_INVALID_ARG for window_depth outside 1..16 or a capacity below *n_windows with
+ * non-zero capacity.
+ */
+dt_status dt_encode_windows(const dt_node *nodes, int32_t n_nodes, int32_t n_features,
+                            int32_t n_classes, int32_t window_depth, int32_t capacity_windows,
+                            int32_t *features, float *thresholds, int32_t *exit_class,
+                            int32_t *exit_leaf, int32_t *n_windows, int32_t *levels);
+
+/*
+ * Validate a tree, encode it for both decompositions and copy the encodings to the
+ * current HIP device.  Synchronous: the upload is complete on return.  The caller keeps
+ * ownership of `nodes`.  The handle owns its device memory and is bound to the device
+ * that was current at creation.
+ * Errors: as dt_tree_check, DT_ERR_HIP, DT_ERR_NO_MEMORY.  *out is set only on DT_OK.
+ */
+dt_status dt_tree_create(const dt_node *nodes, int32_t n_nodes, int32_t n_features,
+                         int32_t n_classes, const dt_tree_options *opt, dt_tree **out);
+
+/* Describe a created tree.  Errors: DT_ERR_INVALID_ARG (null). */
+dt_status dt_tree_get_info(const dt_tree *tree, dt_tree_info *info);
+
+/* Free a tree and its device memory.  NULL is a no-op.  No classify call on the tree may
+ * still be in flight (synchronise its streams first). */
+void dt_tree_destroy(dt_tree *tree);
+
+/*
+ * Classify n records.  Asynchronous on `stream` (a hipStream_t; NULL = the null stream).
+ *   d_x     device pointer, row-major fp32, record r at d_x + r*ld, columns
+ *           0..n_features-1 are read.  Any alignment of 4 bytes; rows that are
+ *           contiguous (ld == n_features), a multiple of 4 floats and 16-byte aligned
+ *           take the vectorised load path.
+ *   n       number of records, >= 0 (0: nothing is launched)
+ *   ld      row stride in floats, >= n_features
+ *   d_out   device pointer to n labels of the type named by out_kind
+ *   algo    DT_ALGO_DATA or DT_ALGO_SPECULATIVE; both give identical results
+ * Exactly n outputs are written; nothing is written on an error return.  Buffers are
+ * owned by the caller and must stay valid until the work on `stream` completes.
+ * Errors: DT_ERR_INVALID_ARG (null tree or pointers with n > 0, n < 0, ld < n_features,
+ * unknown enum, DT_OUT_CLASS_U8 with n_classes > 256, device other than the tree's),
+ * DT_ERR_UNSUPPORTED (n_features > 256, n > 2^37), DT_ERR_HIP (launch failure).
+ * A tree's tables are staged in the LDS when they fit next to the record tiles and are
+ * read from global memory otherwise; every valid tree is supported.
+ */
+dt_status dt_classify(const dt_tree *tree, const float *d_x, int64_t n, int64_t ld,
+                      void *d_out, dt_output out_kind, dt_algo algo, void *stream);
+
+/*
+ * Forest of n_trees trees: tree k occupies nodes[tree_offsets[k] .. tree_offsets[k+1])
+ * with child indices local to that range (each tree is a valid array on its own).
+ * tree_offsets has n_trees + 1 entries, starts at 0 and increases strictly.  All trees
+ * share n_features and n_classes.  Synchronous upload, as dt_tree_create.
+ * Errors: as dt_tree_create; DT_ERR_INVALID_ARG for bad offsets or n_trees < 1;
+ * DT_ERR_UNSUPPORTED for n_trees > 255 or n_classes > 64.
+ */
+dt_status dt_forest_create(const dt_node *nodes, const int32_t *tree_offsets,
+                           int32_t n_trees, int32_t n_features, int32_t n_classes,
+                           const dt_tree_options *opt, dt_forest **out);
+
+/* Free a forest.  NULL is a no-op.  Same in-flight rule as dt_tree_destroy. */
+void dt_forest_destroy(dt_forest *forest);
+
+/*
+ * Majority vote of the forest's trees for n records; ties go to the smallest class id.
+ * Arguments and errors as dt_classify; out_kind must be DT_OUT_CLASS_U8 or
+ * DT_OUT_CLASS_I32.
+ */
+dt_status dt_forest_classify(const dt_forest *forest, const float *d_x, int64_t n, int64_t ld,
+                             void *d_out, dt_output out_kind, dt_algo algo, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DTREE_H */

@@ -1,0 +1,166 @@
+// Tree validation and window encoding (host only).  See encode.hpp.
+#include "encode.hpp"
+
+#include <algorithm>
+#include <cmath>
+#include <limits>
+
+namespace dtree {
+
+dt_status validate_tree(const dt_node *nodes, int32_t n_nodes, int32_t n_features,
+                        int32_t n_classes, TreeShape *shape, std::string *msg) {
+    if (!nodes) { *msg = "nodes is NULL"; return DT_ERR_INVALID_ARG; }
+    if (n_nodes < 1) { *msg = "n_nodes must be >= 1"; return DT_ERR_INVALID_ARG; }
+    if (n_features < 1) { *msg = "n_features must be >= 1"; return DT_ERR_INVALID_ARG; }
+    if (n_classes < 1) { *msg = "n_classes must be >= 1"; return DT_ERR_INVALID_ARG; }
+    if (n_nodes > kMaxNodes) {
+        *msg = "trees are limited to 2^24 nodes";
+        return DT_ERR_UNSUPPORTED;
+    }
+    std::vector<int32_t> parent(n_nodes, -1);
+    int32_t n_internal = 0;
+    for (int32_t i = 0; i < n_nodes; ++i) {
+        const dt_node &n = nodes[i];
+        if (n.cls == -1) {
+            ++n_internal;
+            if (n.feature < 0 || n.feature >= n_features) {
+                *msg = "node " + std::to_string(i) + ": feature " + std::to_string(n.feature) +
+                       " outside [0, n_features)";
+                return DT_ERR_INVALID_TREE;
+            }
+            if (n.left <= i || n.left >= n_nodes - 1) {
+                *msg = "node " + std::to_string(i) + ": left child " + std::to_string(n.left) +
+                       " must satisfy i < left and left + 1 < n_nodes";
+                return DT_ERR_INVALID_TREE;
+            }
+            for (int32_t c = n.left; c <= n.left + 1; ++c) {
+                if (parent[c] != -1) {
+                    *msg = "node " + std::to_string(c) + " has two parents (" +
+                           std::to_string(parent[c]) + " and " + std::to_string(i) + ")";
+                    return DT_ERR_INVALID_TREE;
+                }
+                parent[c] = i;
+            }
+        } else if (n.cls < 0 || n.cls >= n_classes) {
+            *msg = "node " + std::to_string(i) + ": class " + std::to_string(n.cls) +
+                   " outside [0, n_classes) (use -1 for a decision node)";
+            return DT_ERR_INVALID_TREE;
+        }
+    }
+    // With forward edges and single parents every node 1..n-1 hangs below the root; a
+    // full binary tree then has exactly n_nodes = 2 * n_internal + 1.
+    for (int32_t i = 1; i < n_nodes; ++i) {
+        if (parent[i] < 0) {
+            *msg = "node " + std::to_string(i) + " has no parent";
+            return DT_ERR_INVALID_TREE;
+        }
+    }
+    if (n_nodes != 2 * n_internal + 1) {
+        *msg = "not a full binary tree";
+        return DT_ERR_INVALID_TREE;
+    }
+    shape->n_nodes = n_nodes;
+    shape->n_internal = n_internal;
+    shape->n_leaves = n_nodes - n_internal;
+    shape->node_depth.assign(n_nodes, 0);
+    int32_t depth = 0;
+    for (int32_t i = 1; i < n_nodes; ++i) {   // parent index < child index
+        shape->node_depth[i] = shape->node_depth[parent[i]] + 1;
+        depth = std::max(depth, shape->node_depth[i]);
+    }
+    shape->depth = depth;
+    return DT_OK;
+}
+
+int64_t count_windows(const dt_node *nodes, const TreeShape &shape, int depth) {
+    // window roots: the root and every decision node whose depth is a positive multiple
+    // of the window depth
+    int64_t n = 1;
+    for (int32_t i = 1; i < shape.n_nodes; ++i)
+        if (nodes[i].cls == -1 && shape.node_depth[i] % depth == 0) ++n;
+    return n;
+}
+
+int32_t count_levels(const TreeShape &shape, int depth) {
+    // a leaf at depth d is reached in window level ceil(d / D) - 1
+    return std::max(1, (shape.depth + depth - 1) / depth);
+}
+
+void build_windows(const dt_node *nodes, const TreeShape &shape, int depth, WindowTables *out) {
+    const int32_t S = 1 << depth;
+    const float neg_inf = -std::numeric_limits<float>::infinity();
+    out->depth = depth;
+    out->slots = S;
+    out->levels = count_levels(shape, depth);
+    const int64_t nw = count_windows(nodes, shape, depth);
+    out->n_windows = int32_t(nw);
+    out->feature.assign(size_t(nw) * S, 0);
+    out->threshold.assign(size_t(nw) * S, neg_inf);
+    out->exit_class.assign(size_t(nw) * S, -1);
+    out->exit_leaf.assign(size_t(nw) * S, -1);
+
+    std::vector<int32_t> roots;
+    roots.reserve(size_t(nw));
+    roots.push_back(0);
+    std::vector<int32_t> slot_node(size_t(S), -1);
+    for (size_t w = 0; w < roots.size(); ++w) {
+        std::fill(slot_node.begin(), slot_node.end(), -1);
+        slot_node[0] = roots[w];
+        const size_t base = w * size_t(S);
+        // Unreachable exits end the walk like any leaf would; they stay -1.
+        for (int32_t h = 0; h < S - 1; ++h) {
+            const int32_t n = slot_node[size_t(h)];
+            if (n < 0) continue;                          // below an early leaf
+            const int k = 31 - __builtin_clz(uint32_t(h + 1));   // heap level of h
+            if (nodes[n].cls != -1) {
+                // leaf above the bottom: always-right slots lead to this exit
+                const int32_t e = ((h + 2) << (depth - k)) - 2 - (S - 1);
+                out->exit_class[base + size_t(e)] = -(nodes[n].cls + 1);
+                out->exit_leaf[base + size_t(e)] = -(n + 1);
+                continue;
+            }
+            out->feature[base + size_t(h)] = nodes[n].feature;
+            out->threshold[base + size_t(h)] = nodes[n].threshold;
+            for (int32_t b = 0; b < 2; ++b) {
+                const int32_t c = nodes[n].left + b;
+                const int32_t hc = 2 * h + 1 + b;
+                if (hc < S - 1) {
+                    slot_node[size_t(hc)] = c;
+                } else {
+                    const int32_t e = hc - (S - 1);
+                    if (nodes[c].cls != -1) {
+                        out->exit_class[base + size_t(e)] = -(nodes[c].cls + 1);
+                        out->exit_leaf[base + size_t(e)] = -(c + 1);
+                    } else {
+                        const int32_t id = int32_t(roots.size());
+                        roots.push_back(c);
+                        out->exit_class[base + size_t(e)] = id;
+                        out->exit_leaf[base + size_t(e)] = id;
+                    }
+                }
+            }
+        }
+        // A root that is itself a leaf (single-node tree) is handled by the loop above:
+        // slot 0 holds the leaf and its always-right exit is the last one.
+    }
+}
+
+int choose_data_window_depth(const dt_node *nodes, const TreeShape &shape) {
+    const int max_d = std::min(kMaxWindowDepth, std::max(1, shape.depth));
+    int best = 1;
+    int64_t best_bytes = std::numeric_limits<int64_t>::max();
+    for (int d = 1; d <= max_d; ++d) {
+        const int64_t bytes = table_bytes(count_windows(nodes, shape, d), d);
+        if (bytes <= best_bytes) {   // ties: deeper windows, fewer levels
+            best = d;
+            best_bytes = bytes;
+        }
+    }
+    return best;
+}
+
+int choose_spec_window_depth(const TreeShape &shape) {
+    return std::max(1, std::min(4, shape.depth));
+}
+
+}  // namespace dtree

@@ -1,0 +1,65 @@
+// Host-side tree validation and window encoding shared by both GPU decompositions.
+//
+// A window is a block of at most D levels of the tree, rooted at a decision node and
+// embedded in a complete binary heap of 2^D - 1 slots (slot h has children 2h+1, 2h+2).
+// This is the "window" of Section 6 of the paper (evaluate a few levels, then continue
+// from the node reached), and it gives the speculative decomposition its fixed lane map
+// (the processor-node map of Procedure 5): lane h of a record's lane group evaluates
+// slot h.  Slots that hold no decision node (below a leaf that ends the path early)
+// always send the record right, so a leaf met above the bottom is recorded at the exit
+// reached by going right from it; this plays the role of Procedure 5's static leaf
+// paths.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "dtree.h"
+
+namespace dtree {
+
+constexpr int kMaxNodes = 1 << 24;
+constexpr int kMaxWindowDepth = 16;
+constexpr int kMaxSpecWindowDepth = 6;
+
+// Parsed, validated tree.
+struct TreeShape {
+    int32_t n_nodes = 0, n_internal = 0, n_leaves = 0, depth = 0;
+    std::vector<int32_t> node_depth;   // edges from the root
+};
+
+// Validates the layout rules of dtree.h.  Returns DT_OK or an error with `msg` set.
+dt_status validate_tree(const dt_node *nodes, int32_t n_nodes, int32_t n_features,
+                        int32_t n_classes, TreeShape *shape, std::string *msg);
+
+// Window encoding (see dt_encode_windows in dtree.h).  Slot-major arrays of
+// n_windows * 2^depth entries.
+struct WindowTables {
+    int32_t depth = 0;        // D
+    int32_t slots = 0;        // S = 2^D
+    int32_t n_windows = 0;
+    int32_t levels = 0;       // windows on the longest root-to-leaf path
+    std::vector<int32_t> feature;
+    std::vector<float> threshold;
+    std::vector<int32_t> exit_class;
+    std::vector<int32_t> exit_leaf;
+};
+
+// Number of windows for window depth D (without building them).
+int64_t count_windows(const dt_node *nodes, const TreeShape &shape, int depth);
+int32_t count_levels(const TreeShape &shape, int depth);
+
+void build_windows(const dt_node *nodes, const TreeShape &shape, int depth, WindowTables *out);
+
+// Bytes a workgroup stages in LDS for a table of n_windows windows of 2^depth slots:
+// one 8-byte (threshold, feature) pair and one 4-byte exit per slot.
+inline int64_t table_bytes(int64_t n_windows, int depth) {
+    return n_windows * (int64_t(1) << depth) * 12;
+}
+
+// Library's default window depths (see dt_tree_options in dtree.h).
+int choose_data_window_depth(const dt_node *nodes, const TreeShape &shape);
+int choose_spec_window_depth(const TreeShape &shape);
+
+}  // namespace dtree

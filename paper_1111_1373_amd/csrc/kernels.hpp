@@ -1,0 +1,52 @@
+// Interface between the host library (dtree.hip) and the gfx950 kernels (kernels.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace dtree {
+
+constexpr int kTileRows = 64;        // records per wavefront tile (one per lane)
+constexpr int kMaxRowStride = 256;   // LDS row stride limit in floats (n_features <= 256)
+constexpr int kMaxWavesPerBlock = 8;    // kernels are built for <= 512 threads
+
+// Kernel arguments (passed by value).
+struct KArgs {
+    const float *x;          // device features, row-major
+    int64_t n;               // records
+    int64_t ld;              // row stride in floats
+    int64_t n_tiles;         // ceil(n / 64)
+    int32_t n_features;      // F
+    uint32_t magic_f;        // ceil(2^32 / F) for F >= 2 (row = idx / F via mulhi)
+    const int4 *slots;       // n_slots (threshold, feature) pairs, 8 bytes each
+    const int4 *exits;       // n_slots int32 exit codes
+    int32_t slot_bytes;      // LDS bytes of the slot region (multiple of 16)
+    int32_t exit_bytes;      // LDS bytes of the exit region (multiple of 16)
+    int32_t depth;           // window depth D
+    int32_t levels;          // windows on the longest path
+    int32_t waves;           // wavefronts per workgroup
+    int32_t out_kind;        // 0: uint8 output, 1: int32 output
+    void *out;
+};
+
+enum KernelAlgo { kAlgoData = 0, kAlgoSpec = 1 };
+
+// Kernel instance for (algorithm, LDS row stride, vectorised loads, tables staged in the
+// LDS or read from global memory, window depth), or nullptr if no such instance exists.
+// `depth` is ignored by the data kernel.
+const void *kernel_for(int algo, int row_stride, bool vec, bool tables_in_lds, int depth);
+
+// One-time per-instance setup (raise the dynamic LDS limit to the device maximum).
+hipError_t prepare_kernel(const void *fn, int max_lds_bytes);
+
+// Launch: grid of `blocks` workgroups of args.waves wavefronts.
+hipError_t launch_kernel(const void *fn, const KArgs &args, int blocks, int lds_bytes,
+                         hipStream_t stream);
+
+// Dynamic LDS a workgroup of `waves` wavefronts needs.
+inline int lds_bytes_for(int table_bytes, int row_stride, int waves) {
+    return table_bytes + waves * kTileRows * row_stride * 4;
+}
+
+}  // namespace dtree

@@ -1,0 +1,246 @@
+"""Python binding of the C ABI in ``include/dtree.h`` (ctypes; argument marshalling only).
+
+Every evaluation step runs in the gfx950 kernels of ``libdtree.so``; this module only
+converts arguments.  PyTorch supplies device memory and the current stream.  Importing
+this module raises ``ImportError`` if the library has not been built
+(``python -m paper_1111_1373_amd.build``): there is no other code path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+# torch ships its own HIP runtime (same SONAME as ROCm's libamdhip64.so.7).  Load it
+# first so that libdtree.so binds to the very runtime that owns torch's device pointers
+# and streams; two HIP runtimes in one process do not share devices.
+import torch  # noqa: F401
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdtree.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        "libdtree.so is not built; run `python -m paper_1111_1373_amd.build` "
+        "(the GPU library has no fallback)")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+DT_OK, DT_ERR_INVALID_ARG, DT_ERR_INVALID_TREE, DT_ERR_UNSUPPORTED, DT_ERR_HIP, DT_ERR_NO_MEMORY = range(6)
+ALGOS = {"data": 0, "speculative": 1}
+OUT_KINDS = {"class_u8": 0, "class_i32": 1, "leaf_i32": 2}
+
+NODE_DTYPE = np.dtype(
+    [("feature", "<i4"), ("threshold", "<f4"), ("left", "<i4"), ("cls", "<i4")], align=False)
+
+
+class TreeOptions(ctypes.Structure):
+    _fields_ = [("data_window_depth", ctypes.c_int32), ("spec_window_depth", ctypes.c_int32)]
+
+
+class TreeInfo(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "n_nodes", "n_internal", "n_leaves", "depth", "n_features", "n_classes",
+        "data_window_depth", "data_windows", "data_levels",
+        "spec_window_depth", "spec_windows", "spec_levels")] + [
+        ("data_table_bytes", ctypes.c_int64), ("spec_table_bytes", ctypes.c_int64)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
+_p, _i32, _i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+_PROTOS = {
+    "dt_abi_version": (_i32, []),
+    "dt_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "dt_last_error": (ctypes.c_char_p, []),
+    "dt_tree_check": (ctypes.c_int, [_p, _i32, _i32, _i32, _p, _p]),
+    "dt_encode_windows": (ctypes.c_int, [_p, _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p]),
+    "dt_tree_create": (ctypes.c_int, [_p, _i32, _i32, _i32, _p, _p]),
+    "dt_tree_get_info": (ctypes.c_int, [_p, _p]),
+    "dt_tree_destroy": (None, [_p]),
+    "dt_classify": (ctypes.c_int, [_p, _p, _i64, _i64, _p, ctypes.c_int, ctypes.c_int, _p]),
+    "dt_forest_create": (ctypes.c_int, [_p, _p, _i32, _i32, _i32, _p, _p]),
+    "dt_forest_destroy": (None, [_p]),
+    "dt_forest_classify": (ctypes.c_int, [_p, _p, _i64, _i64, _p, ctypes.c_int, ctypes.c_int, _p]),
+    "dt_probe_copy": (ctypes.c_int, [_p, _p, _i64, _p]),
+}
+for _name, (_res, _args) in _PROTOS.items():
+    _f = getattr(_lib, _name)
+    _f.restype = _res
+    _f.argtypes = _args
+
+ABI_VERSION = _lib.dt_abi_version()
+
+
+class DTreeError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        msg = _lib.dt_last_error().decode() or _lib.dt_status_string(status).decode()
+        super().__init__("%s: %s (%s)" % (where, _lib.dt_status_string(status).decode(), msg))
+
+
+def _check(status: int, where: str):
+    if status != DT_OK:
+        raise DTreeError(status, where)
+
+
+def _nodes(nodes) -> np.ndarray:
+    arr = np.ascontiguousarray(nodes)
+    if arr.dtype != NODE_DTYPE:
+        arr = np.ascontiguousarray(arr.astype(NODE_DTYPE))
+    return arr
+
+
+def _options(data_window_depth: int, spec_window_depth: int) -> TreeOptions:
+    return TreeOptions(int(data_window_depth), int(spec_window_depth))
+
+
+def tree_check(nodes, n_features: int, n_classes: int, data_window_depth: int = 0,
+               spec_window_depth: int = 0) -> dict:
+    """Validate a tree on the host and describe its encodings (no GPU needed)."""
+    nd = _nodes(nodes)
+    info = TreeInfo()
+    opt = _options(data_window_depth, spec_window_depth)
+    _check(_lib.dt_tree_check(nd.ctypes.data, len(nd), n_features, n_classes,
+                              ctypes.byref(opt), ctypes.byref(info)), "dt_tree_check")
+    return info.as_dict()
+
+
+def encode_windows(nodes, n_features: int, n_classes: int, window_depth: int) -> dict:
+    """The window tables the kernels use (host only), as numpy arrays of
+    shape [n_windows, 2**window_depth]."""
+    nd = _nodes(nodes)
+    nw, lv = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(_lib.dt_encode_windows(nd.ctypes.data, len(nd), n_features, n_classes, window_depth,
+                                  0, None, None, None, None, ctypes.byref(nw), ctypes.byref(lv)),
+           "dt_encode_windows")
+    s = 1 << window_depth
+    feat = np.empty((nw.value, s), dtype=np.int32)
+    thr = np.empty((nw.value, s), dtype=np.float32)
+    ec = np.empty((nw.value, s), dtype=np.int32)
+    el = np.empty((nw.value, s), dtype=np.int32)
+    _check(_lib.dt_encode_windows(nd.ctypes.data, len(nd), n_features, n_classes, window_depth,
+                                  nw.value, feat.ctypes.data, thr.ctypes.data, ec.ctypes.data,
+                                  el.ctypes.data, ctypes.byref(nw), ctypes.byref(lv)),
+           "dt_encode_windows")
+    return dict(feature=feat, threshold=thr, exit_class=ec, exit_leaf=el, levels=lv.value,
+                n_windows=nw.value, depth=window_depth)
+
+
+def _stream_handle(stream) -> Optional[int]:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def _features_arg(x, n_features: int):
+    import torch
+    if not isinstance(x, torch.Tensor) or x.device.type != "cuda":
+        raise TypeError("features must be a CUDA (HIP) torch tensor")
+    if x.dtype != torch.float32 or x.dim() != 2:
+        raise TypeError("features must be a 2-D float32 tensor")
+    if x.shape[1] < n_features:
+        raise ValueError("features has %d columns, tree needs %d" % (x.shape[1], n_features))
+    if x.stride(1) != 1:
+        raise ValueError("feature rows must be contiguous (stride(1) == 1)")
+    ld = x.stride(0) if x.shape[0] > 1 else max(x.shape[1], n_features)
+    return x.data_ptr(), x.shape[0], ld
+
+
+def _out_tensor(out, n: int, out_kind: str, device):
+    import torch
+    dtype = torch.uint8 if out_kind == "class_u8" else torch.int32
+    if out is None:
+        return torch.empty(n, dtype=dtype, device=device)
+    if out.dtype != dtype or out.numel() != n or not out.is_contiguous() or out.device != device:
+        raise ValueError("out must be a contiguous %s tensor of %d elements on %s" % (dtype, n, device))
+    return out
+
+
+class Tree:
+    """A tree uploaded to the current device (``dt_tree_create``)."""
+
+    def __init__(self, nodes, n_features: int, n_classes: int, data_window_depth: int = 0,
+                 spec_window_depth: int = 0):
+        nd = _nodes(nodes)
+        self.n_features = int(n_features)
+        self.n_classes = int(n_classes)
+        self._h = ctypes.c_void_p()
+        opt = _options(data_window_depth, spec_window_depth)
+        _check(_lib.dt_tree_create(nd.ctypes.data, len(nd), n_features, n_classes,
+                                   ctypes.byref(opt), ctypes.byref(self._h)), "dt_tree_create")
+
+    @property
+    def info(self) -> dict:
+        info = TreeInfo()
+        _check(_lib.dt_tree_get_info(self._h, ctypes.byref(info)), "dt_tree_get_info")
+        return info.as_dict()
+
+    def classify(self, x, algo: str = "data", out_kind: str = "class_u8", out=None, stream=None):
+        """Labels (or leaf indices) of the rows of ``x``; asynchronous on ``stream``
+        (default: torch's current stream)."""
+        ptr, n, ld = _features_arg(x, self.n_features)
+        out = _out_tensor(out, n, out_kind, x.device)
+        _check(_lib.dt_classify(self._h, ptr, n, ld, out.data_ptr() if n else None,
+                                OUT_KINDS[out_kind], ALGOS[algo], _stream_handle(stream)),
+               "dt_classify")
+        return out
+
+    def close(self):
+        if self._h:
+            _lib.dt_tree_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Forest:
+    """A forest uploaded to the current device (``dt_forest_create``)."""
+
+    def __init__(self, nodes, tree_offsets, n_features: int, n_classes: int,
+                 data_window_depth: int = 0, spec_window_depth: int = 0):
+        nd = _nodes(nodes)
+        off = np.ascontiguousarray(tree_offsets, dtype=np.int32)
+        self.n_features = int(n_features)
+        self.n_classes = int(n_classes)
+        self._h = ctypes.c_void_p()
+        opt = _options(data_window_depth, spec_window_depth)
+        _check(_lib.dt_forest_create(nd.ctypes.data, off.ctypes.data, len(off) - 1, n_features,
+                                     n_classes, ctypes.byref(opt), ctypes.byref(self._h)),
+               "dt_forest_create")
+
+    def classify(self, x, algo: str = "data", out_kind: str = "class_u8", out=None, stream=None):
+        ptr, n, ld = _features_arg(x, self.n_features)
+        out = _out_tensor(out, n, out_kind, x.device)
+        _check(_lib.dt_forest_classify(self._h, ptr, n, ld, out.data_ptr() if n else None,
+                                       OUT_KINDS[out_kind], ALGOS[algo], _stream_handle(stream)),
+               "dt_forest_classify")
+        return out
+
+    def close(self):
+        if self._h:
+            _lib.dt_forest_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def probe_copy(src, dst, stream=None):
+    """Streaming copy of ``src`` into ``dst`` (same byte size): counter calibration."""
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != nbytes:
+        raise ValueError("size mismatch")
+    _check(_lib.dt_probe_copy(src.data_ptr(), dst.data_ptr(), nbytes, _stream_handle(stream)),
+           "dt_probe_copy")

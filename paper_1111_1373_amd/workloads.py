@@ -237,6 +237,54 @@ def random_full_tree(rng: np.random.Generator, n_internal: int, n_features: int,
     return nodes
 
 
+def _bfs_nodes(kids, rng, n_features, n_classes, threshold_draw):
+    order, q, h = [], [0], 0
+    while h < len(q):
+        v = q[h]; h += 1
+        order.append(v)
+        if kids[v] is not None:
+            q += list(kids[v])
+    new_id = {v: i for i, v in enumerate(order)}
+    nodes = np.zeros(len(order), dtype=NODE_DTYPE)
+    for v in order:
+        i = new_id[v]
+        if kids[v] is None:
+            nodes[i] = (0, 0.0, -1, int(rng.integers(0, n_classes)))
+        else:
+            nodes[i] = (int(rng.integers(0, n_features)), threshold_draw(), new_id[kids[v][0]], -1)
+    return nodes
+
+
+def paper_shape_tree(rng: np.random.Generator, n_internal: int = 15, depth: int = 11,
+                     n_features: int = 19, n_classes: int = 7) -> np.ndarray:
+    """Random full binary tree with the shape of the paper's experimental tree
+    (Section 4.1: 31 nodes, 16 leaves, depth 11): a root-to-leaf spine of ``depth``
+    decision nodes, whose turns are random, plus ``n_internal - depth`` splits of random
+    leaves above the bottom level, so the depth stays ``depth``."""
+    if n_internal < depth:
+        raise ValueError("need at least `depth` decision nodes")
+    kids = {0: None}
+    dep = {0: 0}
+    nxt = 1
+    v = 0
+    for _ in range(depth):                       # the spine
+        kids[v] = (nxt, nxt + 1)
+        for c in (nxt, nxt + 1):
+            kids[c] = None
+            dep[c] = dep[v] + 1
+        v = nxt + int(rng.integers(0, 2))
+        nxt += 2
+    for _ in range(n_internal - depth):          # side splits that keep the depth
+        leaves = [u for u, k in kids.items() if k is None and dep[u] < depth - 1]
+        u = leaves[int(rng.integers(0, len(leaves)))]
+        kids[u] = (nxt, nxt + 1)
+        for c in (nxt, nxt + 1):
+            kids[c] = None
+            dep[c] = dep[u] + 1
+        nxt += 2
+    return _bfs_nodes(kids, rng, n_features, n_classes, lambda: float(uniform_f32(rng, 1)[0]))
+
+
 def config(k: int, n_samples: Optional[int] = None) -> TreeWorkload:
     """Workload C1..C5 (``k`` in 1..5).  ``n_samples`` may shrink the sample count."""
     seed = SEED_BASE + k

@@ -1,0 +1,259 @@
+"""Host side of the C ABI, on the CPU: exported symbols, tree validation, and the window
+encoding the kernels consume (walked here in numpy and compared with the oracle)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_1111_1373_amd import workloads as W
+from tests import treeutil as TU
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+dt = pytest.importorskip("paper_1111_1373_amd.dtree",
+                         reason="libdtree.so not built (python -m paper_1111_1373_amd.build)")
+
+
+def header_functions():
+    names = []
+    for h in os.listdir(os.path.join(ROOT, "include")):
+        if h.endswith(".h"):
+            src = open(os.path.join(ROOT, "include", h)).read()
+            src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+            names += re.findall(r"\b(dt_\w+)\s*\(", src)
+    return sorted(set(names))
+
+
+def test_every_declared_symbol_is_exported():
+    names = header_functions()
+    assert "dt_classify" in names and "dt_tree_create" in names and "dt_probe_copy" in names
+    out = subprocess.run(["nm", "-D", "--defined-only", dt.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\sT\s(\w+)$", out, re.M))
+    missing = [n for n in names if n not in exported]
+    assert not missing, missing
+    lib = ctypes.CDLL(dt.LIB_PATH)
+    for n in names:
+        getattr(lib, n)
+
+
+def test_abi_version_and_strings():
+    assert dt.ABI_VERSION == 1
+    for s in range(6):
+        assert dt._lib.dt_status_string(s)
+    assert dt._lib.dt_status_string(99) == b"unknown status"
+
+
+def test_node_struct_layout():
+    assert dt.NODE_DTYPE.itemsize == 16
+    assert dt.NODE_DTYPE == W.NODE_DTYPE
+
+
+# ----------------------------------------------------------------------- validation
+
+def _stump():
+    n = np.zeros(3, dtype=W.NODE_DTYPE)
+    n[0] = (0, 0.5, 1, -1)
+    n[1] = (0, 0.0, -1, 0)
+    n[2] = (0, 0.0, -1, 1)
+    return n
+
+
+def _status(nodes, F=2, C=4, **kw):
+    try:
+        dt.tree_check(nodes, F, C, **kw)
+        return dt.DT_OK
+    except dt.DTreeError as e:
+        return e.status
+
+
+def test_valid_trees_pass():
+    assert _status(_stump()) == dt.DT_OK
+    for k in (1, 2, 3, 4):
+        w = W.config(k, n_samples=1)
+        assert _status(w.nodes, w.n_features, w.n_classes) == dt.DT_OK
+
+
+def test_single_leaf_tree():
+    n = np.zeros(1, dtype=W.NODE_DTYPE)
+    n[0] = (0, 0.0, -1, 3)
+    info = dt.tree_check(n, 1, 4)
+    assert info["depth"] == 0 and info["n_internal"] == 0 and info["n_leaves"] == 1
+
+
+@pytest.mark.parametrize("mutate,status", [
+    (lambda n: n.__setitem__(0, (5, 0.5, 1, -1)), "tree"),        # feature out of range
+    (lambda n: n.__setitem__(0, (-1, 0.5, 1, -1)), "tree"),       # negative feature
+    (lambda n: n.__setitem__(1, (0, 0.0, -1, 4)), "tree"),        # class >= n_classes
+    (lambda n: n.__setitem__(1, (0, 0.0, -1, -2)), "tree"),       # class < -1
+    (lambda n: n.__setitem__(0, (0, 0.5, 0, -1)), "tree"),        # self loop
+    (lambda n: n.__setitem__(0, (0, 0.5, 2, -1)), "tree"),        # right child out of range
+    (lambda n: n.__setitem__(1, (0, 0.5, 1, -1)), "tree"),        # back edge / cycle
+])
+def test_invalid_trees_rejected(mutate, status):
+    n = _stump()
+    mutate(n)
+    assert _status(n) == dt.DT_ERR_INVALID_TREE
+
+
+def test_two_parents_rejected():
+    # node 2 and node 1 both claim children 3,4
+    n = np.zeros(5, dtype=W.NODE_DTYPE)
+    n[0] = (0, 0.5, 1, -1)
+    n[1] = (0, 0.5, 3, -1)
+    n[2] = (0, 0.5, 3, -1)
+    n[3] = (0, 0.0, -1, 0)
+    n[4] = (0, 0.0, -1, 0)
+    assert _status(n) == dt.DT_ERR_INVALID_TREE
+
+
+def test_not_full_rejected():
+    n = np.zeros(4, dtype=W.NODE_DTYPE)         # an extra unreachable leaf
+    n[:3] = _stump()
+    n[3] = (0, 0.0, -1, 0)
+    assert _status(n) == dt.DT_ERR_INVALID_TREE
+
+
+def test_argument_errors():
+    n = _stump()
+    assert _status(n, F=0) == dt.DT_ERR_INVALID_ARG
+    assert _status(n, C=0) == dt.DT_ERR_INVALID_ARG
+    assert _status(n, spec_window_depth=7) == dt.DT_ERR_INVALID_ARG
+    assert _status(n, data_window_depth=17) == dt.DT_ERR_INVALID_ARG
+    assert dt._lib.dt_tree_check(None, 3, 2, 4, None, None) == dt.DT_ERR_INVALID_ARG
+    assert dt._lib.dt_tree_check(n.ctypes.data, 0, 2, 4, None, None) == dt.DT_ERR_INVALID_ARG
+    assert b"n_nodes" in dt._lib.dt_last_error()
+    assert dt._lib.dt_tree_destroy(None) is None
+    assert dt._lib.dt_forest_destroy(None) is None
+
+
+def test_non_bfs_order_accepted():
+    """Any order with forward edges and single parents is a valid layout: here node 2's
+    children come before node 1's, which Procedure 1 would not produce."""
+    n = np.zeros(7, dtype=W.NODE_DTYPE)
+    n[0] = (1, 0.5, 1, -1)     # children 1, 2
+    n[1] = (0, 0.25, 5, -1)    # children 5, 6
+    n[2] = (0, 0.75, 3, -1)    # children 3, 4
+    n[3] = (0, 0.0, -1, 0)
+    n[4] = (0, 0.0, -1, 1)
+    n[5] = (0, 0.0, -1, 2)
+    n[6] = (0, 0.0, -1, 3)
+    assert _status(n) == dt.DT_OK
+    x = np.array([[0.1, 0.1], [0.3, 0.1], [0.7, 0.9], [0.8, 0.9]], dtype=np.float32)
+    tab = dt.encode_windows(n, 2, 4, 2)
+    np.testing.assert_array_equal(walk_tables_heap(tab, x), [2, 3, 0, 1])
+    np.testing.assert_array_equal(oracle.tree_classes(n, x, 2), [2, 3, 0, 1])
+
+
+# ----------------------------------------------------------------------- window encoding
+
+def walk_tables_heap(tab, x, exits_key="exit_class"):
+    """Data-decomposition form: per record, D heap steps per window, then the exit."""
+    D = tab["depth"]
+    S = 1 << D
+    n = x.shape[0]
+    rows = np.arange(n)
+    w = np.zeros(n, dtype=np.int64)
+    code = np.full(n, 0, dtype=np.int64)
+    done = np.zeros(n, dtype=bool)
+    for _ in range(tab["levels"]):
+        h = np.zeros(n, dtype=np.int64)
+        for _ in range(D):
+            f = tab["feature"][w, h]
+            t = tab["threshold"][w, h]
+            h = 2 * h + 1 + (~(x[rows, f] < t)).astype(np.int64)
+        c = tab[exits_key][w, h - (S - 1)].astype(np.int64)
+        code = np.where(done, code, c)
+        done |= c < 0
+        w = np.where(done, w, np.maximum(c, 0))
+    assert done.all()
+    return -code - 1
+
+
+def walk_tables_mask(tab, x, exits_key="exit_class"):
+    """Speculative form: evaluate every slot of the window, then walk the bit mask."""
+    D = tab["depth"]
+    S = 1 << D
+    n = x.shape[0]
+    rows = np.arange(n)
+    w = np.zeros(n, dtype=np.int64)
+    code = np.zeros(n, dtype=np.int64)
+    done = np.zeros(n, dtype=bool)
+    for _ in range(tab["levels"]):
+        f = tab["feature"][w]                              # [n, S]
+        t = tab["threshold"][w]
+        bits = ~(x[rows[:, None], f] < t)                  # all slots at once
+        h = np.zeros(n, dtype=np.int64)
+        for _ in range(D):
+            h = 2 * h + 1 + bits[rows, h].astype(np.int64)
+        c = tab[exits_key][w, h - (S - 1)].astype(np.int64)
+        code = np.where(done, code, c)
+        done |= c < 0
+        w = np.where(done, w, np.maximum(c, 0))
+    assert done.all()
+    return -code - 1
+
+
+def _tree_cases():
+    r = np.random.Generator(np.random.PCG64(77))
+    cases = []
+    for t in TU.load_hand_trees():
+        cases.append((t["name"], t["nodes"], t["n_features"], t["n_classes"], t["x"]))
+    for i in range(6):
+        F = int(r.integers(1, 6))
+        n_int = int(r.integers(1, 120))
+        nodes = W.random_full_tree(r, n_int, F, 6, threshold_values=np.concatenate(
+            [TU.special_pool(), W.uniform_f32(r, 8)]))
+        x = W.uniform_f32(r, (3000, F))
+        m = r.random(x.shape) < 0.1
+        pool = TU.special_pool()
+        x[m] = pool[r.integers(0, len(pool), size=int(m.sum()))]
+        cases.append(("random%d" % i, nodes, F, 6, x))
+    w = W.config(3, n_samples=20000)
+    cases.append(("C3", w.nodes, w.n_features, w.n_classes, w.features()))
+    w = W.config(2, n_samples=5000)
+    cases.append(("C2", w.nodes, w.n_features, w.n_classes, w.features()))
+    return cases
+
+
+@pytest.mark.parametrize("case", _tree_cases(), ids=lambda c: c[0])
+@pytest.mark.parametrize("depth", [1, 2, 3, 4, 6, 9])
+def test_window_tables_reproduce_oracle(case, depth):
+    name, nodes, F, C, x = case
+    tab = dt.encode_windows(nodes, F, C, depth)
+    want_cls = oracle.tree_classes(nodes, x, F)
+    want_leaf = oracle.tree_leaves(nodes, x, F)
+    np.testing.assert_array_equal(walk_tables_heap(tab, x), want_cls)
+    np.testing.assert_array_equal(walk_tables_heap(tab, x, "exit_leaf"), want_leaf)
+    if depth <= 6:
+        np.testing.assert_array_equal(walk_tables_mask(tab, x), want_cls)
+        np.testing.assert_array_equal(walk_tables_mask(tab, x, "exit_leaf"), want_leaf)
+
+
+@pytest.mark.parametrize("d,D", [(4, 4), (8, 4), (12, 6), (12, 4), (12, 12), (10, 3), (5, 2)])
+def test_complete_tree_window_counts(d, D):
+    """Complete depth-d tree: windows are rooted at depths 0, D, 2D, ... < d, so there are
+    sum_m 2^(mD) of them, and ceil(d/D) levels."""
+    r = np.random.Generator(np.random.PCG64(d * 100 + D))
+    nodes = W.complete_tree(r, d, 4, 3)
+    tab = dt.encode_windows(nodes, 4, 3, D)
+    assert tab["n_windows"] == sum(1 << (m * D) for m in range(0, (d + D - 1) // D))
+    assert tab["levels"] == -(-d // D)
+    # in a complete window every slot but the padding holds a decision node
+    assert np.isfinite(tab["threshold"][:, :-1]).all() or d % D != 0
+
+
+def test_default_depths_and_info():
+    w = W.config(4, n_samples=1)
+    info = dt.tree_check(w.nodes, w.n_features, w.n_classes)
+    assert info["depth"] == 12 and info["n_internal"] == 4095
+    assert info["spec_window_depth"] == 4 and info["spec_levels"] == 3
+    assert info["data_window_depth"] == 12 and info["data_windows"] == 1
+    assert info["data_table_bytes"] == 4096 * 12
+    w1 = W.config(1, n_samples=1)
+    i1 = dt.tree_check(w1.nodes, w1.n_features, w1.n_classes)
+    assert i1["spec_window_depth"] == 4 and i1["spec_windows"] == 1 and i1["spec_levels"] == 1
