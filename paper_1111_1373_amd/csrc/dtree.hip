@@ -223,12 +223,54 @@ struct dt_tree {
     Plan plan[2][2];              // [algo][vectorised]
 };
 
+namespace {
+
+// Device resources of a forest for one decomposition: all trees' window tables back to
+// back (tree k: slots then class exits, each padded to 16 bytes), the per-tree
+// descriptors {byte_off, slot_bytes, levels, 0} and the LDS chunks
+// {first_tree, end_tree, byte_off, bytes}.
+struct ForestEncoding {
+    int32_t depth = 0;
+    void *d_mem = nullptr;
+    const int4 *d_tables = nullptr, *d_trees = nullptr, *d_chunks = nullptr;
+    std::vector<int4> trees;     // host copy of the descriptors
+    std::vector<int4> chunks;    // host copy of the chunks
+    int64_t table_bytes = 0;
+    int64_t max_tree_bytes = 0;
+    int32_t chunk_lds_bytes = 0; // LDS reserved for one chunk (0: tables read in place)
+    int32_t waves = 0;           // wavefronts per workgroup (one tile each)
+};
+
+void free_forest_encoding(ForestEncoding *e) {
+    if (e->d_mem) (void)hipFree(e->d_mem);
+    e->d_mem = nullptr;
+}
+
+}  // namespace
+
 struct dt_forest {
-    int32_t n_trees = 0;
-    std::vector<dt_tree *> trees;
+    DeviceCaps caps;
+    int32_t n_trees = 0, n_features = 0, n_classes = 0;
+    int row_stride = 0;
+    int vote_words = 0;
+    ForestEncoding enc[2];       // [DT_ALGO_DATA], [DT_ALGO_SPECULATIVE]
+    Plan plan[2][2];             // [algo][vectorised]
 };
 
 namespace {
+
+dtree::Rows make_rows(const float *d_x, int64_t n, int64_t ld, int32_t n_features) {
+    dtree::Rows r{};
+    r.x = d_x;
+    r.n = n;
+    r.ld = ld;
+    r.n_tiles = (n + dtree::kTileRows - 1) / dtree::kTileRows;
+    r.n_features = n_features;
+    r.magic_f = n_features >= 2 ? uint32_t(((uint64_t(1) << 32) + uint64_t(n_features) - 1) /
+                                           uint64_t(n_features))
+                                : 0u;
+    return r;
+}
 
 dt_status classify_impl(const dt_tree *tree, const float *d_x, int64_t n, int64_t ld,
                         void *d_out, dt_output out_kind, dt_algo algo, void *stream) {
@@ -260,15 +302,7 @@ dt_status classify_impl(const dt_tree *tree, const float *d_x, int64_t n, int64_
     const Encoding &enc = tree->enc[algo];
 
     dtree::KArgs a{};
-    a.x = d_x;
-    a.n = n;
-    a.ld = ld;
-    a.n_tiles = (n + dtree::kTileRows - 1) / dtree::kTileRows;
-    a.n_features = tree->n_features;
-    a.magic_f = tree->n_features >= 2
-                    ? uint32_t(((uint64_t(1) << 32) + uint64_t(tree->n_features) - 1) /
-                               uint64_t(tree->n_features))
-                    : 0u;
+    a.in = make_rows(d_x, n, ld, tree->n_features);
     a.slots = enc.d_slots;
     a.exits = out_kind == DT_OUT_LEAF_I32 ? enc.d_exit_leaf : enc.d_exit_class;
     a.slot_bytes = int32_t(enc.slot_bytes);
@@ -278,7 +312,7 @@ dt_status classify_impl(const dt_tree *tree, const float *d_x, int64_t n, int64_
     a.waves = plan.waves;
     a.out_kind = out_kind == DT_OUT_CLASS_U8 ? 0 : 1;
     a.out = d_out;
-    const int64_t want = (a.n_tiles + plan.waves - 1) / plan.waves;
+    const int64_t want = (a.in.n_tiles + plan.waves - 1) / plan.waves;
     const int64_t resident = int64_t(plan.blocks_per_cu) * tree->caps.n_cu;
     const int blocks = int(std::max<int64_t>(1, std::min(want, resident)));
     e = dtree::launch_kernel(plan.fn, a, blocks, plan.lds_bytes,
@@ -334,6 +368,278 @@ void destroy_impl(dt_tree *t) {
     free_encoding(&t->enc[0]);
     free_encoding(&t->enc[1]);
     delete t;
+}
+
+// ---- forests ---------------------------------------------------------------------------
+
+constexpr int kForestSpecDepth = 4;
+
+int vote_words_for(int32_t n_classes) {
+    if (n_classes <= 8) return 2;
+    if (n_classes <= 16) return 4;
+    return 16;
+}
+
+// Encode every tree with window depth `depth` and lay the tables out back to back.
+void encode_forest(const dt_node *nodes, const int32_t *offsets, int32_t n_trees,
+                   const std::vector<dtree::TreeShape> &shapes, int depth,
+                   std::vector<unsigned char> *bytes, ForestEncoding *enc) {
+    enc->depth = depth;
+    enc->trees.assign(size_t(n_trees), int4{0, 0, 0, 0});
+    enc->max_tree_bytes = 0;
+    bytes->clear();
+    for (int32_t k = 0; k < n_trees; ++k) {
+        dtree::WindowTables wt;
+        dtree::build_windows(nodes + offsets[k], shapes[size_t(k)], depth, &wt);
+        const int64_t n_slots = int64_t(wt.n_windows) * wt.slots;
+        const int64_t sb = align16(n_slots * 8), eb = align16(n_slots * 4);
+        const int64_t off = int64_t(bytes->size());
+        bytes->resize(size_t(off + sb + eb), 0);
+        unsigned char *p = bytes->data() + off;
+        for (int64_t i = 0; i < n_slots; ++i) {
+            std::memcpy(p + 8 * i, &wt.threshold[size_t(i)], 4);
+            std::memcpy(p + 8 * i + 4, &wt.feature[size_t(i)], 4);
+        }
+        std::memcpy(p + sb, wt.exit_class.data(), size_t(n_slots * 4));
+        enc->trees[size_t(k)] = int4{int(off), int(sb), wt.levels, 0};
+        enc->max_tree_bytes = std::max(enc->max_tree_bytes, sb + eb);
+    }
+    enc->table_bytes = int64_t(bytes->size());
+}
+
+// Choose the workgroup shape and the LDS chunks of consecutive trees.
+void chunk_forest(const DeviceCaps &caps, int row_stride, ForestEncoding *enc) {
+    const int64_t tile_bytes = int64_t(dtree::kTileRows) * row_stride * 4;
+    enc->chunks.clear();
+    for (int w = dtree::kMaxWavesPerBlock; w >= 1; --w) {
+        const int64_t budget = int64_t(caps.lds_per_block) - w * tile_bytes;
+        if (budget < enc->max_tree_bytes) continue;
+        enc->waves = w;
+        int32_t first = 0;
+        int64_t max_chunk = 0;
+        while (first < int32_t(enc->trees.size())) {
+            int32_t end = first;
+            int64_t bytes = 0;
+            while (end < int32_t(enc->trees.size())) {
+                const int64_t off = enc->trees[size_t(end)].x;
+                const int64_t next = end + 1 < int32_t(enc->trees.size())
+                                         ? int64_t(enc->trees[size_t(end + 1)].x)
+                                         : enc->table_bytes;
+                if (bytes + (next - off) > budget) break;
+                bytes += next - off;
+                ++end;
+            }
+            const int32_t off0 = enc->trees[size_t(first)].x;
+            enc->chunks.push_back(int4{first, end, off0, int(bytes)});
+            max_chunk = std::max(max_chunk, bytes);
+            first = end;
+        }
+        enc->chunk_lds_bytes = int32_t(max_chunk);
+        return;
+    }
+    // single trees too large for the LDS: one pass reading the tables in place
+    enc->waves = 0;
+    enc->chunk_lds_bytes = 0;
+    enc->chunks.push_back(int4{0, int(enc->trees.size()), 0, int(enc->table_bytes)});
+}
+
+dt_status upload_forest(const std::vector<unsigned char> &bytes, ForestEncoding *enc) {
+    const int64_t tb = align16(int64_t(bytes.size()));
+    const int64_t db = int64_t(enc->trees.size()) * 16;
+    const int64_t cb = int64_t(enc->chunks.size()) * 16;
+    std::vector<unsigned char> host(size_t(tb + db + cb), 0);
+    std::memcpy(host.data(), bytes.data(), bytes.size());
+    std::memcpy(host.data() + tb, enc->trees.data(), size_t(db));
+    std::memcpy(host.data() + tb + db, enc->chunks.data(), size_t(cb));
+    hipError_t e = hipMalloc(&enc->d_mem, host.size());
+    if (e != hipSuccess) {
+        enc->d_mem = nullptr;
+        return fail(DT_ERR_NO_MEMORY, std::string("hipMalloc: ") + hipGetErrorString(e));
+    }
+    e = hipMemcpy(enc->d_mem, host.data(), host.size(), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy(forest tables)");
+    auto *base = static_cast<unsigned char *>(enc->d_mem);
+    enc->d_tables = reinterpret_cast<const int4 *>(base);
+    enc->d_trees = reinterpret_cast<const int4 *>(base + tb);
+    enc->d_chunks = reinterpret_cast<const int4 *>(base + tb + db);
+    return DT_OK;
+}
+
+dt_status plan_forest(const DeviceCaps &caps, int algo, int row_stride, bool vec,
+                      int vote_words, const ForestEncoding &enc, Plan *plan) {
+    const bool tab_lds = enc.chunk_lds_bytes > 0;
+    plan->fn = dtree::forest_kernel_for(algo, row_stride, vec, tab_lds, vote_words, enc.depth);
+    if (!plan->fn) {
+        plan->why = "no forest kernel instance for this configuration";
+        return plan->status = DT_ERR_UNSUPPORTED;
+    }
+    {
+        std::lock_guard<std::mutex> lock(g_prep_mutex);
+        if (std::find(g_prepared.begin(), g_prepared.end(), plan->fn) == g_prepared.end()) {
+            hipError_t e = dtree::prepare_kernel(plan->fn, caps.lds_per_block);
+            if (e != hipSuccess) {
+                plan->why = std::string("hipFuncSetAttribute: ") + hipGetErrorString(e);
+                return plan->status = DT_ERR_HIP;
+            }
+            g_prepared.push_back(plan->fn);
+        }
+    }
+    int best_waves = 0;
+    for (int w = 1; w <= dtree::kMaxWavesPerBlock; ++w) {
+        if (tab_lds && w != enc.waves) continue;     // the chunks were cut for enc.waves
+        const int lds = dtree::lds_bytes_for(enc.chunk_lds_bytes, row_stride, w);
+        if (lds > caps.lds_per_block) break;
+        int nb = 0;
+        hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, plan->fn, w * 64,
+                                                                    size_t(lds));
+        if (e != hipSuccess) {
+            plan->why = std::string("hipOccupancyMaxActiveBlocksPerMultiprocessor: ") +
+                        hipGetErrorString(e);
+            return plan->status = DT_ERR_HIP;
+        }
+        if (nb >= 1 && nb * w >= best_waves) {
+            best_waves = nb * w;
+            plan->waves = w;
+            plan->blocks_per_cu = nb;
+            plan->lds_bytes = lds;
+        }
+    }
+    if (best_waves == 0) {
+        plan->why = "no workgroup shape fits this forest kernel";
+        return plan->status = DT_ERR_UNSUPPORTED;
+    }
+    plan->why.clear();
+    return plan->status = DT_OK;
+}
+
+void forest_destroy_impl(dt_forest *f) {
+    if (!f) return;
+    free_forest_encoding(&f->enc[0]);
+    free_forest_encoding(&f->enc[1]);
+    delete f;
+}
+
+dt_status forest_create_impl(const dt_node *nodes, const int32_t *offsets, int32_t n_trees,
+                             int32_t n_features, int32_t n_classes, const dt_tree_options *opt,
+                             dt_forest **out) {
+    if (!out) return fail(DT_ERR_INVALID_ARG, "out is NULL");
+    if (!nodes || !offsets) return fail(DT_ERR_INVALID_ARG, "nodes or tree_offsets is NULL");
+    if (n_trees < 1) return fail(DT_ERR_INVALID_ARG, "n_trees must be >= 1");
+    if (n_features < 1 || n_classes < 1)
+        return fail(DT_ERR_INVALID_ARG, "n_features and n_classes must be >= 1");
+    dt_status st = check_options(opt);
+    if (st != DT_OK) return st;
+    if (opt && opt->spec_window_depth != 0 && opt->spec_window_depth != kForestSpecDepth)
+        return fail(DT_ERR_UNSUPPORTED, "forests use speculative windows of depth 4");
+    if (n_trees > dtree::kMaxForestTrees)
+        return fail(DT_ERR_UNSUPPORTED, "forests are limited to 255 trees");
+    if (n_classes > dtree::kMaxForestClasses)
+        return fail(DT_ERR_UNSUPPORTED, "forests are limited to 64 classes");
+    if (offsets[0] != 0) return fail(DT_ERR_INVALID_ARG, "tree_offsets[0] must be 0");
+    std::vector<dtree::TreeShape> shapes(static_cast<size_t>(n_trees));
+    int max_depth = 0;
+    for (int32_t k = 0; k < n_trees; ++k) {
+        if (offsets[k + 1] <= offsets[k])
+            return fail(DT_ERR_INVALID_ARG, "tree_offsets must increase strictly");
+        std::string msg;
+        st = dtree::validate_tree(nodes + offsets[k], offsets[k + 1] - offsets[k], n_features,
+                                  n_classes, &shapes[size_t(k)], &msg);
+        if (st != DT_OK) return fail(st, "tree " + std::to_string(k) + ": " + msg);
+        max_depth = std::max(max_depth, shapes[size_t(k)].depth);
+    }
+    dt_forest *f = new (std::nothrow) dt_forest();
+    if (!f) return fail(DT_ERR_NO_MEMORY, "host allocation failed");
+    st = query_device(&f->caps);
+    if (st != DT_OK) { delete f; return st; }
+    f->n_trees = n_trees;
+    f->n_features = n_features;
+    f->n_classes = n_classes;
+    f->row_stride = row_stride_for(n_features);
+    f->vote_words = vote_words_for(n_classes);
+
+    // data windows: the depth that makes the forest's tables smallest
+    int data_d = opt && opt->data_window_depth ? opt->data_window_depth : 0;
+    if (!data_d) {
+        int64_t best = -1;
+        for (int d = 1; d <= std::min(dtree::kMaxWindowDepth, std::max(1, max_depth)); ++d) {
+            int64_t total = 0;
+            for (int32_t k = 0; k < n_trees; ++k)
+                total += dtree::table_bytes(
+                    dtree::count_windows(nodes + offsets[k], shapes[size_t(k)], d), d);
+            if (best < 0 || total <= best) { best = total; data_d = d; }
+        }
+    }
+    const int depth[2] = {data_d, kForestSpecDepth};
+    for (int algo = 0; algo < 2; ++algo) {
+        std::vector<unsigned char> bytes;
+        encode_forest(nodes, offsets, n_trees, shapes, depth[algo], &bytes, &f->enc[algo]);
+        if (f->row_stride <= dtree::kMaxRowStride)
+            chunk_forest(f->caps, f->row_stride, &f->enc[algo]);
+        else
+            f->enc[algo].chunks.push_back(int4{0, n_trees, 0, int(f->enc[algo].table_bytes)});
+        if (f->enc[algo].table_bytes > (int64_t(1) << 31) - 1) {
+            forest_destroy_impl(f);
+            return fail(DT_ERR_UNSUPPORTED, "forest tables exceed 2 GiB");
+        }
+        st = upload_forest(bytes, &f->enc[algo]);
+        if (st != DT_OK) { forest_destroy_impl(f); return st; }
+        for (int v = 0; v < 2; ++v) {
+            if (f->row_stride > dtree::kMaxRowStride) {
+                f->plan[algo][v].why = "n_features > 256";
+                continue;
+            }
+            plan_forest(f->caps, algo, f->row_stride, v == 1, f->vote_words, f->enc[algo],
+                        &f->plan[algo][v]);
+        }
+    }
+    *out = f;
+    return DT_OK;
+}
+
+dt_status forest_classify_impl(const dt_forest *f, const float *d_x, int64_t n, int64_t ld,
+                               void *d_out, dt_output out_kind, dt_algo algo, void *stream) {
+    if (!f) return fail(DT_ERR_INVALID_ARG, "forest is NULL");
+    if (n < 0) return fail(DT_ERR_INVALID_ARG, "n must be >= 0");
+    if (algo != DT_ALGO_DATA && algo != DT_ALGO_SPECULATIVE)
+        return fail(DT_ERR_INVALID_ARG, "unknown algo");
+    if (out_kind != DT_OUT_CLASS_U8 && out_kind != DT_OUT_CLASS_I32)
+        return fail(DT_ERR_INVALID_ARG, "forests output classes (uint8 or int32)");
+    if (ld < f->n_features) return fail(DT_ERR_INVALID_ARG, "ld must be >= n_features");
+    if (f->n_features > dtree::kMaxRowStride)
+        return fail(DT_ERR_UNSUPPORTED, "n_features > 256");
+    if (n > (int64_t(1) << 37)) return fail(DT_ERR_UNSUPPORTED, "n > 2^37");
+    if (n == 0) return DT_OK;
+    if (!d_x || !d_out) return fail(DT_ERR_INVALID_ARG, "null device pointer");
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev != f->caps.device)
+        return fail(DT_ERR_INVALID_ARG, "current device differs from the forest's device");
+    const bool vec = (ld == f->n_features) && (f->n_features % 4 == 0) &&
+                     ((reinterpret_cast<uintptr_t>(d_x) & 15u) == 0);
+    const Plan &plan = f->plan[algo][vec ? 1 : 0];
+    if (plan.status != DT_OK) return fail(plan.status, plan.why);
+    const ForestEncoding &enc = f->enc[algo];
+
+    dtree::FArgs a{};
+    a.in = make_rows(d_x, n, ld, f->n_features);
+    a.tables = enc.d_tables;
+    a.trees = enc.d_trees;
+    a.chunks = enc.d_chunks;
+    a.n_trees = f->n_trees;
+    a.n_chunks = int32_t(enc.chunks.size());
+    a.table_lds_bytes = enc.chunk_lds_bytes;
+    a.depth = enc.depth;
+    a.n_classes = f->n_classes;
+    a.waves = plan.waves;
+    a.out_kind = out_kind == DT_OUT_CLASS_U8 ? 0 : 1;
+    a.out = d_out;
+    const int64_t groups = (a.in.n_tiles + plan.waves - 1) / plan.waves;
+    const int64_t resident = int64_t(plan.blocks_per_cu) * f->caps.n_cu;
+    const int blocks = int(std::max<int64_t>(1, std::min(groups, resident)));
+    e = dtree::launch_forest(plan.fn, a, blocks, plan.lds_bytes, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "forest kernel launch");
+    return DT_OK;
 }
 
 }  // namespace
@@ -453,23 +759,26 @@ dt_status dt_classify(const dt_tree *t, const float *d_x, int64_t n, int64_t ld,
 dt_status dt_forest_create(const dt_node *nodes, const int32_t *tree_offsets, int32_t n_trees,
                            int32_t n_features, int32_t n_classes, const dt_tree_options *opt,
                            dt_forest **out) {
-    g_last_error.clear();
-    (void)nodes; (void)tree_offsets; (void)n_trees; (void)n_features; (void)n_classes;
-    (void)opt; (void)out;
-    return fail(DT_ERR_UNSUPPORTED, "forests are not implemented yet");
+    try {
+        g_last_error.clear();
+        return forest_create_impl(nodes, tree_offsets, n_trees, n_features, n_classes, opt, out);
+    } catch (const std::bad_alloc &) {
+        return fail(DT_ERR_NO_MEMORY, "host allocation failed");
+    } catch (...) {
+        return fail(DT_ERR_INVALID_ARG, "unexpected internal error");
+    }
 }
 
-void dt_forest_destroy(dt_forest *f) {
-    if (!f) return;
-    for (dt_tree *t : f->trees) destroy_impl(t);
-    delete f;
-}
+void dt_forest_destroy(dt_forest *f) { forest_destroy_impl(f); }
 
 dt_status dt_forest_classify(const dt_forest *f, const float *d_x, int64_t n, int64_t ld,
                              void *d_out, dt_output out_kind, dt_algo algo, void *stream) {
-    g_last_error.clear();
-    (void)f; (void)d_x; (void)n; (void)ld; (void)d_out; (void)out_kind; (void)algo; (void)stream;
-    return fail(DT_ERR_UNSUPPORTED, "forests are not implemented yet");
+    try {
+        g_last_error.clear();
+        return forest_classify_impl(f, d_x, n, ld, d_out, out_kind, algo, stream);
+    } catch (...) {
+        return fail(DT_ERR_INVALID_ARG, "unexpected internal error");
+    }
 }
 
 }  // extern "C"

@@ -1,0 +1,182 @@
+// gfx950 forest kernel: majority vote of many trees over every record.
+//
+// Forests are evaluated tree after tree (the concatenated-trees scheme the paper cites
+// in Section 1) and the trees' classes are combined by majority vote, ties going to the
+// smallest class id.  Each record's votes live in registers as packed 8-bit counters.
+//
+// The tables of all trees together usually exceed the LDS, so a workgroup works on one
+// group of tiles at a time (one 64-record tile per wavefront, staged once) and streams the
+// trees' tables through the LDS in chunks of consecutive trees; every tree of a chunk is
+// walked for the whole group before the next chunk replaces it.  All wavefronts of a
+// workgroup iterate over the same groups and chunks, so the workgroup barriers around the
+// chunk copies are reached uniformly.  Forests whose single trees do not fit the LDS read
+// their tables from global memory instead.
+#include "device_common.hpp"
+
+namespace dtree {
+namespace {
+
+using dev::Slot;
+
+template <int NV>
+__device__ __forceinline__ void add_vote(uint32_t (&votes)[NV], int cls) {
+    const int word = cls >> 2;
+    const uint32_t inc = 1u << ((cls & 3) * 8);
+#pragma unroll
+    for (int r = 0; r < NV; ++r) votes[r] += (word == r) ? inc : 0u;
+}
+
+// Class with the most votes; the strict comparison keeps the smallest id on ties.
+template <int NV>
+__device__ __forceinline__ int majority(const uint32_t (&votes)[NV], int n_classes) {
+    int best = 0;
+    int best_count = -1;
+#pragma unroll
+    for (int r = 0; r < NV; ++r) {
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const int c = r * 4 + b;
+            const int count = int((votes[r] >> (8 * b)) & 255u);
+            if (c < n_classes && count > best_count) {
+                best_count = count;
+                best = c;
+            }
+        }
+    }
+    return best;
+}
+
+// SD = 0: data decomposition; SD > 0: speculative decomposition with window depth SD.
+template <int RS, bool VEC, bool TAB_LDS, int NV, int SD>
+__global__ void __launch_bounds__(512) forest_kernel(FArgs a) {
+    extern __shared__ int4 lds[];
+    constexpr bool kPrefetch = VEC && RS <= 64;
+    const int wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    float *tile = reinterpret_cast<float *>(lds) + wave * (kTileRows * RS);
+    int4 *tab = lds + (a.waves * kTileRows * RS) / 4;   // chunk buffer after the tiles
+    const float *row = tile + lane * RS;
+    const int sw = dev::swz<RS>(lane);
+    const int64_t n_groups = (a.in.n_tiles + a.waves - 1) / a.waves;
+
+    // Exit code of this lane's record for the tree whose tables start at `base`.
+    auto eval_tree = [&](const char *base, int levels, int slot_bytes) -> int32_t {
+        const Slot *sl = reinterpret_cast<const Slot *>(base);
+        const int32_t *ex = reinterpret_cast<const int32_t *>(base + slot_bytes);
+        if constexpr (SD == 0) {
+            return dev::walk_data(sl, ex, a.depth, levels, row, sw);
+        } else {
+            const dev::Spec<RS, SD> spec(lane);
+            const Slot root = sl[spec.j];
+            return spec.run(sl, ex, levels, root, tile);
+        }
+    };
+
+    int64_t g = blockIdx.x;
+    dev::VecTile<(kPrefetch ? RS : 4)> buf;
+    if constexpr (kPrefetch) {
+        const int64_t t0 = g * a.waves + wave;
+        if (g < n_groups && t0 < a.in.n_tiles) buf.load(a.in, t0, lane);
+    }
+    for (; g < n_groups; g += gridDim.x) {
+        const int64_t t = g * a.waves + wave;
+        const bool active = t < a.in.n_tiles;        // uniform per wavefront
+        dev::wave_sync();
+        if (active) {
+            if constexpr (kPrefetch)
+                buf.store(a.in, tile, lane);
+            else
+                dev::stage_now<RS, VEC>(a.in, tile, t, lane);
+        }
+        dev::wave_sync();
+        if constexpr (kPrefetch) {
+            const int64_t tn = t + int64_t(gridDim.x) * a.waves;
+            if (tn < a.in.n_tiles) buf.load(a.in, tn, lane);
+        }
+
+        uint32_t votes[NV];
+#pragma unroll
+        for (int r = 0; r < NV; ++r) votes[r] = 0u;
+        for (int c = 0; c < a.n_chunks; ++c) {
+            const int4 ch = a.chunks[c];             // {first, end, byte_off, bytes}
+            if constexpr (TAB_LDS) {
+                __syncthreads();                     // previous chunk no longer read
+                const int4 *src = a.tables + (ch.z >> 4);
+                for (int i = threadIdx.x; i < (ch.w >> 4); i += blockDim.x) tab[i] = src[i];
+                __syncthreads();
+                if (active) {
+                    const char *cbase = reinterpret_cast<const char *>(tab);
+                    for (int k = ch.x; k < ch.y; ++k) {
+                        const int4 d = a.trees[k];   // {byte_off, slot_bytes, levels, 0}
+                        add_vote(votes, ~eval_tree(cbase + (d.x - ch.z), d.z, d.y));
+                    }
+                }
+            } else {
+                if (active) {
+                    const char *gbase = reinterpret_cast<const char *>(a.tables);
+                    for (int k = ch.x; k < ch.y; ++k) {
+                        const int4 d = a.trees[k];
+                        add_vote(votes, ~eval_tree(gbase + d.x, d.z, d.y));
+                    }
+                }
+            }
+        }
+        if (active)
+            dev::store_value(a.out, a.out_kind, a.in.n, t * kTileRows + lane,
+                             majority(votes, a.n_classes));
+    }
+}
+
+template <int RS, bool VEC, bool TAB_LDS, int NV>
+const void *for_votes(int algo, int depth) {
+    if (algo == kAlgoData)
+        return reinterpret_cast<const void *>(&forest_kernel<RS, VEC, TAB_LDS, NV, 0>);
+    if (depth == 4)
+        return reinterpret_cast<const void *>(&forest_kernel<RS, VEC, TAB_LDS, NV, 4>);
+    return nullptr;
+}
+
+template <int RS, bool VEC, bool TAB_LDS>
+const void *for_tab(int algo, int vote_words, int depth) {
+    switch (vote_words) {
+        case 2: return for_votes<RS, VEC, TAB_LDS, 2>(algo, depth);
+        case 4: return for_votes<RS, VEC, TAB_LDS, 4>(algo, depth);
+        case 16: return for_votes<RS, VEC, TAB_LDS, 16>(algo, depth);
+        default: return nullptr;
+    }
+}
+
+template <int RS>
+const void *for_stride(int algo, bool vec, bool tab_lds, int vote_words, int depth) {
+    if (vec)
+        return tab_lds ? for_tab<RS, true, true>(algo, vote_words, depth)
+                       : for_tab<RS, true, false>(algo, vote_words, depth);
+    return tab_lds ? for_tab<RS, false, true>(algo, vote_words, depth)
+                   : for_tab<RS, false, false>(algo, vote_words, depth);
+}
+
+}  // namespace
+
+const void *forest_kernel_for(int algo, int row_stride, bool vec, bool tables_in_lds,
+                              int vote_words, int depth) {
+    switch (row_stride) {
+        case 4: return for_stride<4>(algo, vec, tables_in_lds, vote_words, depth);
+        case 8: return for_stride<8>(algo, vec, tables_in_lds, vote_words, depth);
+        case 16: return for_stride<16>(algo, vec, tables_in_lds, vote_words, depth);
+        case 32: return for_stride<32>(algo, vec, tables_in_lds, vote_words, depth);
+        case 64: return for_stride<64>(algo, vec, tables_in_lds, vote_words, depth);
+        case 128: return for_stride<128>(algo, vec, tables_in_lds, vote_words, depth);
+        case 256: return for_stride<256>(algo, vec, tables_in_lds, vote_words, depth);
+        default: return nullptr;
+    }
+}
+
+hipError_t launch_forest(const void *fn, const FArgs &args, int blocks, int lds_bytes,
+                         hipStream_t stream) {
+    FArgs a = args;
+    void *params[] = {&a};
+    return hipLaunchKernel(fn, dim3(unsigned(blocks)), dim3(unsigned(args.waves * 64)), params,
+                           size_t(lds_bytes), stream);
+}
+
+}  // namespace dtree

@@ -7,25 +7,51 @@
 
 namespace dtree {
 
-constexpr int kTileRows = 64;        // records per wavefront tile (one per lane)
-constexpr int kMaxRowStride = 256;   // LDS row stride limit in floats (n_features <= 256)
-constexpr int kMaxWavesPerBlock = 8;    // kernels are built for <= 512 threads
+constexpr int kTileRows = 64;          // records per wavefront tile (one per lane)
+constexpr int kMaxRowStride = 256;     // LDS row stride limit in floats (n_features <= 256)
+constexpr int kMaxWavesPerBlock = 8;   // kernels are built for <= 512 threads
+constexpr int kMaxForestTrees = 255;   // 8-bit vote counters
+constexpr int kMaxForestClasses = 64;  // 16 VGPRs of packed counters
 
-// Kernel arguments (passed by value).
-struct KArgs {
+// The record matrix a kernel reads.
+struct Rows {
     const float *x;          // device features, row-major
     int64_t n;               // records
     int64_t ld;              // row stride in floats
     int64_t n_tiles;         // ceil(n / 64)
     int32_t n_features;      // F
     uint32_t magic_f;        // ceil(2^32 / F) for F >= 2 (row = idx / F via mulhi)
+};
+
+// Single-tree kernel arguments (passed by value).
+struct KArgs {
+    Rows in;
     const int4 *slots;       // n_slots (threshold, feature) pairs, 8 bytes each
     const int4 *exits;       // n_slots int32 exit codes
-    int32_t slot_bytes;      // LDS bytes of the slot region (multiple of 16)
-    int32_t exit_bytes;      // LDS bytes of the exit region (multiple of 16)
+    int32_t slot_bytes;      // bytes of the slot region (multiple of 16)
+    int32_t exit_bytes;      // bytes of the exit region (multiple of 16)
     int32_t depth;           // window depth D
     int32_t levels;          // windows on the longest path
     int32_t waves;           // wavefronts per workgroup
+    int32_t out_kind;        // 0: uint8 output, 1: int32 output
+    void *out;
+};
+
+// Forest kernel arguments.  Tree k's tables are the bytes [off_k, off_k + slot_bytes_k)
+// (slots) followed by its exit codes, inside `tables`; trees[k] = {off_k, slot_bytes_k,
+// levels_k, 0}.  Chunks are runs of consecutive trees staged into the LDS together:
+// chunks[c] = {first_tree, end_tree, byte_off, bytes}.
+struct FArgs {
+    Rows in;
+    const int4 *tables;
+    const int4 *trees;
+    const int4 *chunks;
+    int32_t n_trees;
+    int32_t n_chunks;
+    int32_t table_lds_bytes; // LDS bytes reserved for one chunk (0: tables read in place)
+    int32_t depth;           // window depth D (every tree)
+    int32_t n_classes;
+    int32_t waves;
     int32_t out_kind;        // 0: uint8 output, 1: int32 output
     void *out;
 };
@@ -37,11 +63,18 @@ enum KernelAlgo { kAlgoData = 0, kAlgoSpec = 1 };
 // `depth` is ignored by the data kernel.
 const void *kernel_for(int algo, int row_stride, bool vec, bool tables_in_lds, int depth);
 
+// Forest kernel instance; `vote_words` = 32-bit words of packed 8-bit counters
+// (1, 2, 4, 8 or 16 for up to 4, 8, 16, 32 or 64 classes).
+const void *forest_kernel_for(int algo, int row_stride, bool vec, bool tables_in_lds,
+                              int vote_words, int depth);
+
 // One-time per-instance setup (raise the dynamic LDS limit to the device maximum).
 hipError_t prepare_kernel(const void *fn, int max_lds_bytes);
 
-// Launch: grid of `blocks` workgroups of args.waves wavefronts.
+// Launches: grid of `blocks` workgroups of args.waves wavefronts.
 hipError_t launch_kernel(const void *fn, const KArgs &args, int blocks, int lds_bytes,
+                         hipStream_t stream);
+hipError_t launch_forest(const void *fn, const FArgs &args, int blocks, int lds_bytes,
                          hipStream_t stream);
 
 // Dynamic LDS a workgroup of `waves` wavefronts needs.

@@ -257,3 +257,30 @@ def test_default_depths_and_info():
     w1 = W.config(1, n_samples=1)
     i1 = dt.tree_check(w1.nodes, w1.n_features, w1.n_classes)
     assert i1["spec_window_depth"] == 4 and i1["spec_windows"] == 1 and i1["spec_levels"] == 1
+
+
+# ----------------------------------------------------------------------- forests (host checks)
+
+def _forest_status(nodes, offsets, F=2, C=4, spec_depth=0):
+    h = ctypes.c_void_p()
+    nd = np.ascontiguousarray(nodes)
+    off = np.ascontiguousarray(offsets, dtype=np.int32)
+    opt = dt.TreeOptions(0, spec_depth)
+    return dt._lib.dt_forest_create(nd.ctypes.data, off.ctypes.data, len(off) - 1, F, C,
+                                    ctypes.byref(opt), ctypes.byref(h))
+
+
+def test_forest_argument_errors():
+    s = _stump()
+    two = np.concatenate([s, s])
+    assert _forest_status(two, [0, 3, 6], spec_depth=5) == dt.DT_ERR_UNSUPPORTED
+    assert _forest_status(two, [1, 3, 6]) == dt.DT_ERR_INVALID_ARG          # offsets[0] != 0
+    assert _forest_status(two, [0, 3, 3]) == dt.DT_ERR_INVALID_ARG          # empty tree
+    assert _forest_status(two, [0]) == dt.DT_ERR_INVALID_ARG                # no trees
+    assert _forest_status(two, [0, 3, 6], C=65) == dt.DT_ERR_UNSUPPORTED    # > 64 classes
+    many = np.concatenate([s] * 256)
+    assert _forest_status(many, np.arange(0, 3 * 257, 3)) == dt.DT_ERR_UNSUPPORTED
+    bad = two.copy()
+    bad[4] = (0, 0.0, -1, 9)                                                # class >= C
+    assert _forest_status(bad, [0, 3, 6]) == dt.DT_ERR_INVALID_TREE
+    assert b"tree 1" in dt._lib.dt_last_error()

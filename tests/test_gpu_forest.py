@@ -1,0 +1,107 @@
+"""GPU parity of the forest majority vote (both decompositions) against the CPU oracle."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_1111_1373_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+ALGOS = ["data", "speculative"]
+
+
+@pytest.fixture(scope="module")
+def dt():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_1111_1373_amd import dtree
+    return dtree
+
+
+def _forest(trees):
+    off = np.zeros(len(trees) + 1, dtype=np.int32)
+    off[1:] = np.cumsum([len(t) for t in trees])
+    return np.concatenate(trees), off
+
+
+def _check(dt, nodes, off, x, F, C, algos=ALGOS, xd=None):
+    want = oracle.forest_classes(nodes, off, x, F, C)
+    f = dt.Forest(nodes, off, F, C)
+    xd = torch.from_numpy(np.ascontiguousarray(x)).cuda() if xd is None else xd
+    for algo in algos:
+        got = f.classify(xd, algo=algo, out_kind="class_i32").cpu().numpy()
+        np.testing.assert_array_equal(got, want, err_msg=algo)
+        if C <= 256:
+            got8 = f.classify(xd, algo=algo, out_kind="class_u8").cpu().numpy()
+            np.testing.assert_array_equal(got8.astype(np.int32), want, err_msg=algo + "/u8")
+
+
+def test_config5_full_size(dt):
+    w = W.config(5)
+    x = w.features()
+    print("C5", x.shape, flush=True)
+    _check(dt, w.nodes, w.tree_offsets, x, w.n_features, w.n_classes)
+
+
+@pytest.mark.parametrize("votes", [[2, 1, 2], [1, 2], [0, 3, 3, 5, 5], [7], [4, 4, 0, 0],
+                                   [6, 5, 6, 5, 5], list(range(8)) * 4])
+def test_vote_ties(dt, votes):
+    trees = []
+    for c in votes:
+        n = np.zeros(1, dtype=W.NODE_DTYPE)
+        n[0] = (0, 0.0, -1, c)
+        trees.append(n)
+    nodes, off = _forest(trees)
+    x = W.uniform_f32(np.random.Generator(np.random.PCG64(0)), (300, 4))
+    _check(dt, nodes, off, x, 4, 8)
+
+
+@pytest.mark.parametrize("C", [1, 2, 5, 8, 9, 16, 17, 33, 64])
+def test_class_counts(dt, C):
+    r = np.random.Generator(np.random.PCG64(C))
+    trees = [W.complete_tree(r, int(r.integers(1, 7)), 12, C) for _ in range(int(r.integers(3, 20)))]
+    nodes, off = _forest(trees)
+    x = W.uniform_f32(r, (5000, 12))
+    _check(dt, nodes, off, x, 12, C)
+
+
+@pytest.mark.parametrize("n_trees", [1, 2, 31, 255])
+def test_tree_counts_and_shapes(dt, n_trees):
+    r = np.random.Generator(np.random.PCG64(100 + n_trees))
+    trees = [W.random_full_tree(r, int(r.integers(0, 60)), 19, 7) for _ in range(n_trees)]
+    nodes, off = _forest(trees)
+    x = W.uniform_f32(r, (3001, 19))        # F = 19: general (non-vectorised) staging
+    _check(dt, nodes, off, x, 19, 7)
+
+
+def test_large_trees_read_tables_in_place(dt):
+    """Trees whose tables do not fit the LDS: the forest reads them from global memory."""
+    r = np.random.Generator(np.random.PCG64(7))
+    trees = [W.random_full_tree(r, 8191, 16, 10) for _ in range(3)]
+    nodes, off = _forest(trees)
+    x = W.uniform_f32(r, (4000, 16))
+    _check(dt, nodes, off, x, 16, 10)
+
+
+@pytest.mark.parametrize("n", [1, 63, 65, 130, 1000, 70000])
+def test_ragged_sizes_and_strides(dt, n):
+    w = W.config(5, n_samples=n)
+    x = w.features()
+    _check(dt, w.nodes, w.tree_offsets, x, w.n_features, w.n_classes)
+    padded = torch.zeros((n, w.n_features + 3), dtype=torch.float32, device="cuda")
+    padded[:, :w.n_features] = torch.from_numpy(x).cuda()
+    _check(dt, w.nodes, w.tree_offsets, x, w.n_features, w.n_classes,
+           xd=padded[:, :w.n_features])
+
+
+def test_forest_argument_errors(dt):
+    w = W.config(5, n_samples=10)
+    f = dt.Forest(w.nodes, w.tree_offsets, w.n_features, w.n_classes)
+    x = torch.from_numpy(w.features()).cuda()
+    with pytest.raises(dt.DTreeError):
+        f.classify(x, out_kind="leaf_i32")
+    out = torch.empty(10, dtype=torch.uint8, device="cuda")
+    assert dt._lib.dt_forest_classify(f._h, x.data_ptr(), 10, 31, out.data_ptr(), 0, 0, None) == dt.DT_ERR_INVALID_ARG
+    assert dt._lib.dt_forest_classify(f._h, x.data_ptr(), 0, 32, out.data_ptr(), 0, 0, None) == dt.DT_OK
