@@ -5,7 +5,8 @@
 
 A step is one classify call over the whole workload with features resident in HBM:
 feature tiles HBM -> LDS, the tree walk (data or speculative decomposition) and the label
-write.  The tree is uploaded once before timing.  The default workload is C4
+write (for the forest workload C5: every tree's walk and the majority vote).  The tree is
+uploaded once before timing.  The default workload is C4
 (16,777,216 records x 64 fp32 features, complete depth-12 tree, 32 classes).  Both
 decompositions are timed; ``value`` is the faster one.  The GPU labels of every timed
 configuration are checked bit-exact against the CPU oracle on all records, and the
@@ -35,7 +36,8 @@ PAPER_CONTEXT = {"speculative_us": 404.466, "data_us": 538.235, "ratio": 404.466
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("kernels.hip", "kernels.hpp", "dtree.hip", "encode.cpp"):
+    for f in ("kernels.hip", "kernels.hpp", "forest.hip", "device_common.hpp", "dtree.hip",
+              "encode.cpp", "encode.hpp"):
         with open(os.path.join(ROOT, "paper_1111_1373_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -65,7 +67,7 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=4, choices=[1, 2, 3, 4])
+    ap.add_argument("--config", type=int, default=4, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--algos", default="data,speculative")
     ap.add_argument("--spec-window-depth", type=int, default=0)
     ap.add_argument("--data-window-depth", type=int, default=0)
@@ -96,10 +98,20 @@ def main() -> int:
     n, F = x_np.shape
     log("features", x_np.shape)
     x = torch.from_numpy(x_np).cuda()
-    tree = dt.Tree(w.nodes, w.n_features, w.n_classes, data_window_depth=args.data_window_depth,
-                   spec_window_depth=args.spec_window_depth)
-    info = tree.info
-    log("tree", info)
+    if w.is_forest:
+        tree = dt.Forest(w.nodes, w.tree_offsets, w.n_features, w.n_classes,
+                         data_window_depth=args.data_window_depth,
+                         spec_window_depth=args.spec_window_depth)
+        info = {"n_trees": len(w.tree_offsets) - 1, "data_window_depth": "auto",
+                "spec_window_depth": 4}
+        oracle_call = lambda: oracle.forest_classes(w.nodes, w.tree_offsets, x_np, F, w.n_classes)
+    else:
+        tree = dt.Tree(w.nodes, w.n_features, w.n_classes,
+                       data_window_depth=args.data_window_depth,
+                       spec_window_depth=args.spec_window_depth)
+        info = tree.info
+        oracle_call = lambda: oracle.tree_classes(w.nodes, x_np, F)
+    log("model", info)
 
     # oracle: parity reference and CPU baseline (single core, serial C walk)
     want = None
@@ -108,7 +120,7 @@ def main() -> int:
     budget = args.cpu_seconds if not args.no_cpu_baseline else 0.0
     while True:
         t0 = time.perf_counter()
-        res = oracle.tree_classes(w.nodes, x_np, F)
+        res = oracle_call()
         t_or.append(time.perf_counter() - t0)
         if want is None:
             want = res
@@ -155,6 +167,8 @@ def main() -> int:
             "mismatches_vs_oracle": mism,
             "window_depth": info["data_window_depth" if algo == "data" else "spec_window_depth"],
         }
+        if w.is_forest:
+            results[algo]["tree_samples_per_s"] = results[algo]["samples_per_s"] * info["n_trees"]
         log(algo, json.dumps(results[algo]))
         if mism:
             log("PARITY FAILURE:", algo, mism, "mismatches")
@@ -184,7 +198,8 @@ def main() -> int:
                      "frac": achieved / PEAK_HBM_GBPS,
                      "traffic": traffic,
                      "algorithmic_bytes_per_launch": algo_bytes,
-                     "kernel": "%s_kernel" % ("data" if best == "data" else "spec")},
+                     "kernel": ("forest_kernel(%s)" % best) if w.is_forest
+                               else "%s_kernel" % ("data" if best == "data" else "spec")},
         "cpu_baseline": cpu,
         "parity": "bit-exact vs oracle on all %d records" % n
                   if all(v["mismatches_vs_oracle"] == 0 for v in results.values())
