@@ -71,6 +71,7 @@ def main() -> int:
     ap.add_argument("--algos", default="data,speculative")
     ap.add_argument("--spec-window-depth", type=int, default=0)
     ap.add_argument("--data-window-depth", type=int, default=0)
+    ap.add_argument("--waves-per-cu", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU time spent timing the oracle")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -101,14 +102,16 @@ def main() -> int:
     if w.is_forest:
         tree = dt.Forest(w.nodes, w.tree_offsets, w.n_features, w.n_classes,
                          data_window_depth=args.data_window_depth,
-                         spec_window_depth=args.spec_window_depth)
+                         spec_window_depth=args.spec_window_depth,
+                         waves_per_cu=args.waves_per_cu)
         info = {"n_trees": len(w.tree_offsets) - 1, "data_window_depth": "auto",
                 "spec_window_depth": 4}
         oracle_call = lambda: oracle.forest_classes(w.nodes, w.tree_offsets, x_np, F, w.n_classes)
     else:
         tree = dt.Tree(w.nodes, w.n_features, w.n_classes,
                        data_window_depth=args.data_window_depth,
-                       spec_window_depth=args.spec_window_depth)
+                       spec_window_depth=args.spec_window_depth,
+                       waves_per_cu=args.waves_per_cu)
         info = tree.info
         oracle_call = lambda: oracle.tree_classes(w.nodes, x_np, F)
     log("model", info)
@@ -169,6 +172,8 @@ def main() -> int:
         }
         if w.is_forest:
             results[algo]["tree_samples_per_s"] = results[algo]["samples_per_s"] * info["n_trees"]
+        else:
+            results[algo]["launch"] = tree.launch_info(x, algo=algo, out_kind="class_u8")
         log(algo, json.dumps(results[algo]))
         if mism:
             log("PARITY FAILURE:", algo, mism, "mismatches")

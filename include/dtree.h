@@ -91,6 +91,9 @@ typedef struct dt_forest dt_forest;
 typedef struct {
     int32_t data_window_depth;
     int32_t spec_window_depth;
+    int32_t waves_per_cu;      /* launch tuning: resident wavefronts per compute unit
+                                  (0 = the library's choice, about 64 KiB of record tiles in
+                                  flight per CU); limited by the LDS and registers */
 } dt_tree_options;
 
 /* Shape of a tree and of its two encodings. */
@@ -128,12 +131,13 @@ dt_status dt_tree_check(const dt_node *nodes, int32_t n_nodes, int32_t n_feature
 /*
  * Window encoding used by the GPU kernels, written to caller-owned host buffers.  Host
  * only.  Window w occupies slots [w*2^d, (w+1)*2^d) of each array (d = window_depth):
- *   features[], thresholds[]  slot h < 2^d - 1 is heap position h of the window (children
- *                   2h+1, 2h+2); a slot that holds no decision node has feature 0 and
- *                   threshold -inf, so it always sends a record right.  Slot 2^d - 1 is
+ *   features[], thresholds[]  slot p in [1, 2^d) is node p of the window's heap, stored
+ *                   1-based: the window root is slot 1 and the children of slot p are
+ *                   slots 2p and 2p+1.  A slot that holds no decision node has feature 0
+ *                   and threshold -inf, so it always sends a record right.  Slot 0 is
  *                   padding with the same values.
  *   exit_class[], exit_leaf[]  entry e is the outcome of leaving the window at bottom
- *                   position e (heap position 2^d - 1 + e): a value v >= 0 is the window
+ *                   position e (heap position 2^d + e): a value v >= 0 is the window
  *                   to continue in; v < 0 ends the walk with class (resp. leaf index)
  *                   -v - 1.  A leaf met above the bottom level is recorded at the exit
  *                   reached by always going right from it.
@@ -164,6 +168,23 @@ dt_status dt_tree_get_info(const dt_tree *tree, dt_tree_info *info);
 /* Free a tree and its device memory.  NULL is a no-op.  No classify call on the tree may
  * still be in flight (synchronise its streams first). */
 void dt_tree_destroy(dt_tree *tree);
+
+/* Launch shape dt_classify uses for one (algorithm, output, input layout).  Diagnostic. */
+typedef struct {
+    int32_t waves_per_workgroup;
+    int32_t workgroups_per_cu;     /* resident workgroups per compute unit               */
+    int32_t lds_bytes;             /* dynamic LDS per workgroup                          */
+    int32_t result_buffer_tiles;   /* tiles of 64 results each wavefront buffers        */
+    int32_t tables_in_lds;         /* 1: tree tables staged in the LDS, 0: read in place */
+    int32_t load_mode;             /* 0: scalar loads, 1: 16-byte loads, 2: 16-byte loads
+                                      of rows exactly one LDS row stride wide            */
+} dt_launch_info;
+
+/* Fill *info with the launch shape of dt_classify(tree, d_x, n, ld, ..., out_kind, algo)
+ * for any n > 0.  Only the alignment of d_x is read.  Errors: DT_ERR_INVALID_ARG (null,
+ * unknown enum, ld < n_features), or the error classify would return for this shape. */
+dt_status dt_tree_launch_info(const dt_tree *tree, const float *d_x, int64_t ld,
+                              dt_output out_kind, dt_algo algo, dt_launch_info *info);
 
 /*
  * Classify n records.  Asynchronous on `stream` (a hipStream_t; NULL = the null stream).

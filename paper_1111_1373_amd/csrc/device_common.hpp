@@ -6,9 +6,9 @@
 // a tree (where every lane reads the same feature) are conflict-free, and the 16-byte
 // staging stores land on distinct banks.
 //
-// Window tables (built on the host, see encode.hpp): for window w, slot h holds the
-// (threshold, feature) of heap position h; exit e holds the next window (>= 0) or the
-// result -(value + 1).
+// Window tables (built on the host, see encode.hpp): for window w, slot p in [1, 2^D)
+// holds the (threshold, feature) of heap node p (children 2p, 2p+1; slot 0 is padding);
+// exit e holds the next window (>= 0) or the result -(value + 1).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -26,6 +26,11 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 struct alignas(8) Slot {
     float t;
     int32_t f;
+};
+
+// The two children 2p, 2p+1 of a heap slot: one aligned 16-byte LDS read.
+struct alignas(16) Slot2 {
+    Slot l, r;
 };
 
 template <int RS>
@@ -69,36 +74,73 @@ __device__ __forceinline__ void put4(float *tile, int r, int c, f32x4 v) {
 
 // Vectorised staging (ld == F, F % 4 == 0, 16-byte aligned base), one tile held in
 // registers so that the next tile's loads overlap the walk of the current one.
-template <int RS>
+//
+// Loads are never guarded by a branch: guarded loads compile into branches whose joins
+// copy the loaded registers, which forces a wait for every outstanding load right after
+// the prefetch is issued.  A lane whose vector lies past the tile's valid data re-reads
+// the last valid vector instead, so rows past the end of the input hold copies of valid
+// features; their results are never stored.  EXACT (F == RS): every lane owns RS/4
+// vectors of a full tile and the LDS positions are shifts and masks.
+template <int RS, bool EXACT>
 struct VecTile {
     static constexpr int kVec = RS / 4;   // 16-byte vectors per lane for F == RS
     f32x4 v[kVec];
 
-    __device__ __forceinline__ void load(const Rows &in, int64_t tile, int lane) {
-        const int nvec = (valid_rows(in, tile) * in.n_features) >> 2;
-        const f32x4 *src = reinterpret_cast<const f32x4 *>(in.x + tile * kTileRows * in.n_features);
+    __device__ __forceinline__ const f32x4 *base(const Rows &in, int64_t tile) const {
+        return reinterpret_cast<const f32x4 *>(in.x + tile * kTileRows * in.n_features);
+    }
+
+    // Any tile; nvec = vectors holding valid records (>= 1).
+    __device__ __forceinline__ void load_clamped(const Rows &in, int64_t tile, int lane, int nvec) {
+        const f32x4 *src = base(in, tile);
 #pragma unroll
         for (int k = 0; k < kVec; ++k) {
             const int q = k * 64 + lane;
-            v[k] = q < nvec ? __builtin_nontemporal_load(src + q) : f32x4{0.f, 0.f, 0.f, 0.f};
+            v[k] = __builtin_nontemporal_load(src + (q < nvec ? q : nvec - 1));
         }
     }
 
-    __device__ __forceinline__ void store(const Rows &in, float *tile, int lane) const {
-        const int full = kTileRows * in.n_features / 4;
+    // Tile with 64 valid records.
+    __device__ __forceinline__ void load_full(const Rows &in, int64_t tile, int lane) {
+        if constexpr (EXACT) {
+            const f32x4 *src = base(in, tile) + lane;
 #pragma unroll
-        for (int k = 0; k < kVec; ++k) {
-            const int q = k * 64 + lane;
-            if (q < full) {
-                const uint32_t e = uint32_t(q) * 4u;
-                const int r = int(div_f(e, in));
-                put4<RS>(tile, r, int(e) - r * in.n_features, v[k]);
+            for (int k = 0; k < kVec; ++k) v[k] = __builtin_nontemporal_load(src + k * 64);
+        } else {
+            load_clamped(in, tile, lane, kTileRows * in.n_features / 4);
+        }
+    }
+
+    // Any tile, including the partial last one.
+    __device__ __forceinline__ void load_tail(const Rows &in, int64_t tile, int lane) {
+        load_clamped(in, tile, lane, (valid_rows(in, tile) * in.n_features) >> 2);
+    }
+
+    __device__ __forceinline__ void store(const Rows &in, float *tile, int lane) const {
+        if constexpr (EXACT) {
+            constexpr int sh = __builtin_ctz(RS);
+#pragma unroll
+            for (int k = 0; k < kVec; ++k) {
+                const int e = (k * 64 + lane) * 4;
+                put4<RS>(tile, e >> sh, e & (RS - 1), v[k]);
+            }
+        } else {
+            const int full = kTileRows * in.n_features / 4;
+#pragma unroll
+            for (int k = 0; k < kVec; ++k) {
+                const int q = k * 64 + lane;
+                if (q < full) {
+                    const uint32_t e = uint32_t(q) * 4u;
+                    const int r = int(div_f(e, in));
+                    put4<RS>(tile, r, int(e) - r * in.n_features, v[k]);
+                }
             }
         }
     }
 };
 
-// Vectorised staging of wide rows (RS > 64) in chunks of 16 vectors per lane.
+// Vectorised staging of wide rows (RS > 64) in chunks of 16 vectors per lane, without
+// prefetch (loads clamped to the valid vectors as in VecTile).
 template <int RS>
 __device__ __forceinline__ void stage_wide(const Rows &in, float *tile, int64_t t, int lane) {
     const int nvec = (valid_rows(in, t) * in.n_features) >> 2;
@@ -110,7 +152,7 @@ __device__ __forceinline__ void stage_wide(const Rows &in, float *tile, int64_t 
 #pragma unroll
         for (int k = 0; k < 16; ++k) {
             const int q = (k0 + k) * 64 + lane;
-            v[k] = q < nvec ? __builtin_nontemporal_load(src + q) : f32x4{0.f, 0.f, 0.f, 0.f};
+            v[k] = __builtin_nontemporal_load(src + (q < nvec ? q : nvec - 1));
         }
 #pragma unroll
         for (int k = 0; k < 16; ++k) {
@@ -140,13 +182,13 @@ __device__ __forceinline__ void stage_scalar(const Rows &in, float *tile, int64_
 }
 
 // Stage tile t without register prefetch.
-template <int RS, bool VEC>
+template <int RS, int LOAD>
 __device__ __forceinline__ void stage_now(const Rows &in, float *tile, int64_t t, int lane) {
-    if constexpr (VEC && RS <= 64) {
-        VecTile<RS> buf;
-        buf.load(in, t, lane);
+    if constexpr (LOAD != kLoadScalar && RS <= 64) {
+        VecTile<RS, LOAD == kLoadExact> buf;
+        buf.load_tail(in, t, lane);
         buf.store(in, tile, lane);
-    } else if constexpr (VEC) {
+    } else if constexpr (LOAD != kLoadScalar) {
         stage_wide<RS>(in, tile, t, lane);
     } else {
         stage_scalar<RS>(in, tile, t, lane);
@@ -154,26 +196,87 @@ __device__ __forceinline__ void stage_now(const Rows &in, float *tile, int64_t t
 }
 
 // ---- data decomposition: the record of this lane walks one tree --------------------------
-// Within a window: h <- 2h + 1 + !(x[f_h] < t_h) for exactly D steps (Procedure 2's
-// child + predicate step in heap form); then the exit names the next window or the result.
+// Within a window the record descends p <- 2p + !(x[f_p] < t_p) for exactly D steps
+// (Procedure 2's "child + predicate" step on the 1-based heap), then the exit names the next
+// window or the result.  One-level lookahead: while node p's feature is read, both children
+// of p are fetched as one 16-byte pair and the comparison selects between them, so each
+// level costs one LDS round trip instead of two dependent ones.
 __device__ __forceinline__ int32_t walk_data(const Slot *slots, const int32_t *exits, int D,
                                              int levels, const float *row, int sw) {
-    const int last = (1 << D) - 1;
+    const int S = 1 << D;
     int w = 0;
     int32_t code = -1;
     for (int level = 0; level < levels; ++level) {
-        const int base = w << D;
-        int h = 0;
-        for (int k = 0; k < D; ++k) {
-            const Slot s = slots[base + h];
+        const Slot *win = slots + (w << D);
+        int p = 1;
+        Slot s = win[1];
+        for (int k = 1; k < D; ++k) {
             const float xv = row[s.f ^ sw];
-            h = 2 * h + 1 + int(!(xv < s.t));
+            const Slot2 kids = *reinterpret_cast<const Slot2 *>(win + 2 * p);
+            const bool right = !(xv < s.t);
+            p = 2 * p + int(right);
+            s = right ? kids.r : kids.l;
         }
-        code = exits[base + h - last];
+        const float xv = row[s.f ^ sw];
+        p = 2 * p + int(!(xv < s.t));
+        code = exits[(w << D) + p - S];
         if (code < 0) break;
         w = code;
     }
     return code;
+}
+
+// Data decomposition over K trees at once (forests): the K walks of one record are
+// independent, so interleaving them keeps K LDS dependency chains in flight per lane.
+// Tree i's tables start at base[i]; all trees share the window depth D.
+template <int K>
+__device__ __forceinline__ void walk_data_k(const char *const (&base)[K], const int (&slot_bytes)[K],
+                                            const int (&levels)[K], int D, const float *row,
+                                            int sw, int32_t (&code)[K]) {
+    const int S = 1 << D;
+    int w[K];
+    int max_levels = 0;
+#pragma unroll
+    for (int i = 0; i < K; ++i) {
+        w[i] = 0;
+        code[i] = 0;
+        max_levels = levels[i] > max_levels ? levels[i] : max_levels;
+    }
+    for (int level = 0; level < max_levels; ++level) {
+        const Slot *win[K];
+        int p[K];
+        Slot s[K];
+#pragma unroll
+        for (int i = 0; i < K; ++i) {
+            win[i] = reinterpret_cast<const Slot *>(base[i]) + (w[i] << D);
+            p[i] = 1;
+            s[i] = win[i][1];
+        }
+        for (int k = 1; k < D; ++k) {
+#pragma unroll
+            for (int i = 0; i < K; ++i) {
+                const float xv = row[s[i].f ^ sw];
+                const Slot2 kids = *reinterpret_cast<const Slot2 *>(win[i] + 2 * p[i]);
+                const bool right = !(xv < s[i].t);
+                p[i] = 2 * p[i] + int(right);
+                s[i] = right ? kids.r : kids.l;
+            }
+        }
+        bool all_done = true;
+#pragma unroll
+        for (int i = 0; i < K; ++i) {
+            const float xv = row[s[i].f ^ sw];
+            p[i] = 2 * p[i] + int(!(xv < s[i].t));
+            if (code[i] >= 0 && level < levels[i]) {
+                const int32_t *ex = reinterpret_cast<const int32_t *>(base[i] + slot_bytes[i]);
+                const int32_t c = ex[(w[i] << D) + p[i] - S];
+                code[i] = c;
+                if (c >= 0) w[i] = c;
+            }
+            all_done = all_done && code[i] < 0;
+        }
+        if (__all(all_done)) break;
+    }
 }
 
 // ---- speculative decomposition: a tile of 64 records through one tree -------------------
@@ -186,7 +289,7 @@ template <int RS, int D>
 struct Spec {
     static constexpr int S = 1 << D;
     using Bits = typename std::conditional<(S > 32), uint64_t, uint32_t>::type;
-    int j;          // slot evaluated by this lane
+    int j;          // slot evaluated by this lane (slot 0 is padding)
     int seg_shift;  // first lane of this lane's segment
 
     __device__ __forceinline__ explicit Spec(int lane)
@@ -219,11 +322,12 @@ struct Spec {
         return bits;
     }
 
+    // Exit index reached from the window root (slot 1) by following the bits: p <- 2p + b_p.
     __device__ __forceinline__ int walk(Bits bits) const {
-        int h = 0;
+        int p = 1;
 #pragma unroll
-        for (int k = 0; k < D; ++k) h = 2 * h + 1 + int((bits >> h) & 1);
-        return h - (S - 1);
+        for (int k = 0; k < D; ++k) p = 2 * p + int((bits >> p) & 1);
+        return p - S;
     }
 
     // Exit code of every lane's record.  `root` = slots[j] of window 0.  All 64 lanes

@@ -50,6 +50,7 @@ struct DeviceCaps {
     int device = -1;
     int n_cu = 0;
     int lds_per_block = 0;
+    int lds_per_cu = 0;
 };
 
 dt_status query_device(DeviceCaps *caps) {
@@ -60,6 +61,9 @@ dt_status query_device(DeviceCaps *caps) {
     e = hipDeviceGetAttribute(&caps->lds_per_block, hipDeviceAttributeMaxSharedMemoryPerBlock,
                               caps->device);
     if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute(LDS)");
+    e = hipDeviceGetAttribute(&caps->lds_per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
+                              caps->device);
+    if (e != hipSuccess || caps->lds_per_cu < caps->lds_per_block) caps->lds_per_cu = caps->lds_per_block;
     return DT_OK;
 }
 
@@ -104,6 +108,8 @@ dt_status check_options(const dt_tree_options *opt) {
         return fail(DT_ERR_INVALID_ARG, "data_window_depth must be 0 (auto) or 1..16");
     if (opt->spec_window_depth < 0 || opt->spec_window_depth > dtree::kMaxSpecWindowDepth)
         return fail(DT_ERR_INVALID_ARG, "spec_window_depth must be 0 (auto) or 1..6");
+    if (opt->waves_per_cu < 0 || opt->waves_per_cu > 32)
+        return fail(DT_ERR_INVALID_ARG, "waves_per_cu must be 0 (auto) or 1..32");
     return DT_OK;
 }
 
@@ -142,6 +148,8 @@ struct Plan {
     int waves = 0;
     int blocks_per_cu = 0;
     int lds_bytes = 0;
+    int out_cap = 0;          // single-tree kernels: result tiles buffered per wavefront
+    int tables_in_lds = 0;
     dt_status status = DT_ERR_UNSUPPORTED;
     std::string why;
 };
@@ -149,67 +157,95 @@ struct Plan {
 std::mutex g_prep_mutex;
 std::vector<const void *> g_prepared;
 
-// Plan for one kernel instance with the tables either in the LDS or in global memory.
-dt_status plan_variant(const DeviceCaps &caps, int algo, int row_stride, bool vec, int depth,
-                       bool tab_lds, int64_t table_bytes, Plan *plan) {
-    plan->fn = dtree::kernel_for(algo, row_stride, vec, tab_lds, depth);
-    if (!plan->fn) {
-        plan->why = "no kernel instance for this configuration";
-        return plan->status = DT_ERR_UNSUPPORTED;
+// Wavefronts per CU the library aims for (measured on MI355X).  The data decomposition is
+// HBM-bound once about 64 KiB of record tiles are in flight per CU; more wavefronts only
+// add contention.  The speculative decomposition, which does 2^D times the lane work per
+// record, runs best with 8 wavefronts per CU on every tile width (fewer leave its LDS
+// latency exposed, more slow it down).
+int target_waves_per_cu(int algo, int row_stride) {
+    if (algo == DT_ALGO_SPECULATIVE) return 8;
+    const int tile_bytes = dtree::kTileRows * row_stride * 4;
+    return std::max(2, std::min(32, (64 * 1024) / tile_bytes));
+}
+
+void prepare_once(const void *fn, int lds_limit, Plan *plan) {
+    std::lock_guard<std::mutex> lock(g_prep_mutex);
+    if (std::find(g_prepared.begin(), g_prepared.end(), fn) != g_prepared.end()) return;
+    hipError_t e = dtree::prepare_kernel(fn, lds_limit);
+    if (e != hipSuccess) {
+        plan->why = std::string("hipFuncSetAttribute: ") + hipGetErrorString(e);
+        plan->status = DT_ERR_HIP;
+        return;
     }
-    const int lds_tables = tab_lds ? int(table_bytes) : 0;
-    {
-        std::lock_guard<std::mutex> lock(g_prep_mutex);
-        if (std::find(g_prepared.begin(), g_prepared.end(), plan->fn) == g_prepared.end()) {
-            hipError_t e = dtree::prepare_kernel(plan->fn, caps.lds_per_block);
-            if (e != hipSuccess) {
-                plan->why = std::string("hipFuncSetAttribute: ") + hipGetErrorString(e);
-                return plan->status = DT_ERR_HIP;
-            }
-            g_prepared.push_back(plan->fn);
-        }
-    }
-    int best_waves = 0;
-    for (int w = 1; w <= dtree::kMaxWavesPerBlock; ++w) {
-        const int lds = dtree::lds_bytes_for(lds_tables, row_stride, w);
-        if (lds > caps.lds_per_block) break;
-        int nb = 0;
-        hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, plan->fn, w * 64,
-                                                                    size_t(lds));
-        if (e != hipSuccess) {
-            plan->why = std::string("hipOccupancyMaxActiveBlocksPerMultiprocessor: ") +
-                        hipGetErrorString(e);
-            return plan->status = DT_ERR_HIP;
-        }
-        if (nb < 1) continue;
-        if (nb * w >= best_waves) {   // ties: larger workgroups share one table copy
-            best_waves = nb * w;
-            plan->waves = w;
-            plan->blocks_per_cu = nb;
-            plan->lds_bytes = lds;
-        }
-    }
-    if (best_waves == 0) {
-        plan->why = "no workgroup shape fits this kernel";
-        return plan->status = DT_ERR_UNSUPPORTED;
-    }
-    plan->why.clear();
-    return plan->status = DT_OK;
+    g_prepared.push_back(fn);
 }
 
 // Tables stay in the LDS when that still leaves room for kMinLdsWaves wavefront tiles per
 // workgroup; larger trees read their tables from global memory.
 constexpr int kMinLdsWaves = 2;
+constexpr int kMaxOutCap = 256;
 
-dt_status make_plan(const DeviceCaps &caps, int algo, int row_stride, bool vec, int depth,
-                    int64_t table_bytes, Plan *plan) {
-    if (dtree::lds_bytes_for(0, row_stride, 1) > caps.lds_per_block) {
+// Single-tree plan: workgroup shape, resident workgroups per CU and the result buffer, for
+// results of `out_bytes` bytes (1 or 4).
+dt_status make_plan(const DeviceCaps &caps, int algo, int row_stride, int load_mode, int depth,
+                    int64_t table_bytes, int out_bytes, int waves_per_cu, Plan *plan) {
+    const int tile_bytes = dtree::kTileRows * row_stride * 4;
+    const int res_bytes = dtree::kTileRows * out_bytes;   // one tile of results
+    if (tile_bytes + res_bytes > caps.lds_per_block) {
         plan->why = "one record tile exceeds the workgroup LDS";
         return plan->status = DT_ERR_UNSUPPORTED;
     }
-    const bool fits = table_bytes + int64_t(kMinLdsWaves) * dtree::kTileRows * row_stride * 4 <=
-                      caps.lds_per_block;
-    return plan_variant(caps, algo, row_stride, vec, depth, fits, table_bytes, plan);
+    const bool tab_lds =
+        table_bytes + int64_t(kMinLdsWaves) * (tile_bytes + res_bytes) <= caps.lds_per_block;
+    const int table_lds = tab_lds ? int(table_bytes) : 0;
+    plan->tables_in_lds = tab_lds ? 1 : 0;
+    plan->fn = dtree::kernel_for(algo, row_stride, load_mode, tab_lds, depth);
+    if (!plan->fn) {
+        plan->why = "no kernel instance for this configuration";
+        return plan->status = DT_ERR_UNSUPPORTED;
+    }
+    plan->status = DT_OK;
+    prepare_once(plan->fn, caps.lds_per_block, plan);
+    if (plan->status != DT_OK) return plan->status;
+
+    const int target = waves_per_cu > 0 ? waves_per_cu : target_waves_per_cu(algo, row_stride);
+    // Try every workgroup size and count per CU; keep the shape reaching the most resident
+    // wavefronts up to the target (registers and the LDS both limit residency); on ties
+    // prefer larger workgroups (fewer table copies), then a larger result buffer.
+    int best = 0, best_cap = 0;
+    for (int w = std::min(dtree::kMaxWavesPerBlock, target); w >= 1; --w) {
+        for (int bpc = (target + w - 1) / w; bpc >= 1; --bpc) {
+            const int budget = std::min(caps.lds_per_block, caps.lds_per_cu / bpc);
+            if (table_lds + w * (tile_bytes + res_bytes) > budget) continue;
+            const int cap =
+                std::min(kMaxOutCap, (budget - table_lds - w * tile_bytes) / (w * res_bytes));
+            const int lds = dtree::lds_bytes_for(table_lds, row_stride, w, cap * res_bytes);
+            int nb = 0;
+            hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, plan->fn, w * 64,
+                                                                        size_t(lds));
+            if (e != hipSuccess) {
+                plan->why = std::string("hipOccupancyMaxActiveBlocksPerMultiprocessor: ") +
+                            hipGetErrorString(e);
+                return plan->status = DT_ERR_HIP;
+            }
+            const int blocks = std::min(nb, bpc);
+            const int score = std::min(target, blocks * w);
+            if (blocks >= 1 && (score > best || (score == best && w == plan->waves && cap > best_cap))) {
+                best = score;
+                best_cap = cap;
+                plan->waves = w;
+                plan->blocks_per_cu = blocks;
+                plan->lds_bytes = lds;
+                plan->out_cap = cap;
+            }
+        }
+    }
+    if (best == 0) {
+        plan->why = "tables and one record tile exceed the workgroup LDS";
+        return plan->status = DT_ERR_UNSUPPORTED;
+    }
+    plan->why.clear();
+    return plan->status = DT_OK;
 }
 
 }  // namespace
@@ -220,7 +256,7 @@ struct dt_tree {
     int32_t n_features = 0, n_classes = 0;
     int row_stride = 0;
     Encoding enc[2];              // [DT_ALGO_DATA], [DT_ALGO_SPECULATIVE]
-    Plan plan[2][2];              // [algo][vectorised]
+    Plan plan[2][dtree::kLoadModes][2];   // [algo][load mode][uint8 / int32 results]
 };
 
 namespace {
@@ -254,10 +290,18 @@ struct dt_forest {
     int row_stride = 0;
     int vote_words = 0;
     ForestEncoding enc[2];       // [DT_ALGO_DATA], [DT_ALGO_SPECULATIVE]
-    Plan plan[2][2];             // [algo][vectorised]
+    Plan plan[2][dtree::kLoadModes];  // [algo][load mode]
 };
 
 namespace {
+
+// The fastest record-tile load path the layout of the features allows.
+int load_mode_for(const float *d_x, int64_t ld, int32_t n_features, int row_stride) {
+    const bool dense = ld == n_features && n_features % 4 == 0 &&
+                       (reinterpret_cast<uintptr_t>(d_x) & 15u) == 0;
+    if (!dense) return dtree::kLoadScalar;
+    return n_features == row_stride ? dtree::kLoadExact : dtree::kLoadVec;
+}
 
 dtree::Rows make_rows(const float *d_x, int64_t n, int64_t ld, int32_t n_features) {
     dtree::Rows r{};
@@ -295,9 +339,8 @@ dt_status classify_impl(const dt_tree *tree, const float *d_x, int64_t n, int64_
     if (dev != tree->caps.device)
         return fail(DT_ERR_INVALID_ARG, "current device differs from the tree's device");
 
-    const bool vec = (ld == tree->n_features) && (tree->n_features % 4 == 0) &&
-                     ((reinterpret_cast<uintptr_t>(d_x) & 15u) == 0);
-    const Plan &plan = tree->plan[algo][vec ? 1 : 0];
+    const Plan &plan = tree->plan[algo][load_mode_for(d_x, ld, tree->n_features, tree->row_stride)]
+                                 [out_kind == DT_OUT_CLASS_U8 ? 0 : 1];
     if (plan.status != DT_OK) return fail(plan.status, plan.why);
     const Encoding &enc = tree->enc[algo];
 
@@ -311,6 +354,8 @@ dt_status classify_impl(const dt_tree *tree, const float *d_x, int64_t n, int64_
     a.levels = enc.levels;
     a.waves = plan.waves;
     a.out_kind = out_kind == DT_OUT_CLASS_U8 ? 0 : 1;
+    a.out_cap = plan.out_cap;
+    a.out_vec = (reinterpret_cast<uintptr_t>(d_out) & 15u) == 0 ? 1 : 0;
     a.out = d_out;
     const int64_t want = (a.in.n_tiles + plan.waves - 1) / plan.waves;
     const int64_t resident = int64_t(plan.blocks_per_cu) * tree->caps.n_cu;
@@ -350,13 +395,17 @@ dt_status create_impl(const dt_node *nodes, int32_t n_nodes, int32_t n_features,
             delete t;
             return st;
         }
-        for (int v = 0; v < 2; ++v) {
+        for (int m = 0; m < dtree::kLoadModes; ++m) {
             if (t->row_stride > dtree::kMaxRowStride) {
-                t->plan[algo][v].why = "n_features > 256";
+                t->plan[algo][m][0].why = t->plan[algo][m][1].why = "n_features > 256";
                 continue;
             }
-            make_plan(t->caps, algo, t->row_stride, v == 1, t->enc[algo].depth,
-                      t->enc[algo].table_bytes(), &t->plan[algo][v]);
+            if (m == dtree::kLoadExact && n_features != t->row_stride) continue;
+            if (m != dtree::kLoadScalar && n_features % 4 != 0) continue;
+            for (int o = 0; o < 2; ++o)
+                make_plan(t->caps, algo, t->row_stride, m, t->enc[algo].depth,
+                          t->enc[algo].table_bytes(), o == 0 ? 1 : 4,
+                          opt ? opt->waves_per_cu : 0, &t->plan[algo][m][o]);
         }
     }
     *out = t;
@@ -465,10 +514,11 @@ dt_status upload_forest(const std::vector<unsigned char> &bytes, ForestEncoding 
     return DT_OK;
 }
 
-dt_status plan_forest(const DeviceCaps &caps, int algo, int row_stride, bool vec,
+dt_status plan_forest(const DeviceCaps &caps, int algo, int row_stride, int load_mode,
                       int vote_words, const ForestEncoding &enc, Plan *plan) {
     const bool tab_lds = enc.chunk_lds_bytes > 0;
-    plan->fn = dtree::forest_kernel_for(algo, row_stride, vec, tab_lds, vote_words, enc.depth);
+    plan->fn = dtree::forest_kernel_for(algo, row_stride, load_mode, tab_lds, vote_words,
+                                        enc.depth);
     if (!plan->fn) {
         plan->why = "no forest kernel instance for this configuration";
         return plan->status = DT_ERR_UNSUPPORTED;
@@ -583,13 +633,15 @@ dt_status forest_create_impl(const dt_node *nodes, const int32_t *offsets, int32
         }
         st = upload_forest(bytes, &f->enc[algo]);
         if (st != DT_OK) { forest_destroy_impl(f); return st; }
-        for (int v = 0; v < 2; ++v) {
+        for (int m = 0; m < dtree::kLoadModes; ++m) {
             if (f->row_stride > dtree::kMaxRowStride) {
-                f->plan[algo][v].why = "n_features > 256";
+                f->plan[algo][m].why = "n_features > 256";
                 continue;
             }
-            plan_forest(f->caps, algo, f->row_stride, v == 1, f->vote_words, f->enc[algo],
-                        &f->plan[algo][v]);
+            if (m == dtree::kLoadExact && n_features != f->row_stride) continue;
+            if (m != dtree::kLoadScalar && n_features % 4 != 0) continue;
+            plan_forest(f->caps, algo, f->row_stride, m, f->vote_words, f->enc[algo],
+                        &f->plan[algo][m]);
         }
     }
     *out = f;
@@ -615,9 +667,7 @@ dt_status forest_classify_impl(const dt_forest *f, const float *d_x, int64_t n, 
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
     if (dev != f->caps.device)
         return fail(DT_ERR_INVALID_ARG, "current device differs from the forest's device");
-    const bool vec = (ld == f->n_features) && (f->n_features % 4 == 0) &&
-                     ((reinterpret_cast<uintptr_t>(d_x) & 15u) == 0);
-    const Plan &plan = f->plan[algo][vec ? 1 : 0];
+    const Plan &plan = f->plan[algo][load_mode_for(d_x, ld, f->n_features, f->row_stride)];
     if (plan.status != DT_OK) return fail(plan.status, plan.why);
     const ForestEncoding &enc = f->enc[algo];
 
@@ -745,6 +795,27 @@ dt_status dt_tree_get_info(const dt_tree *t, dt_tree_info *info) {
 }
 
 void dt_tree_destroy(dt_tree *t) { destroy_impl(t); }
+
+dt_status dt_tree_launch_info(const dt_tree *t, const float *d_x, int64_t ld, dt_output out_kind,
+                              dt_algo algo, dt_launch_info *info) {
+    g_last_error.clear();
+    if (!t || !info) return fail(DT_ERR_INVALID_ARG, "null argument");
+    if (algo != DT_ALGO_DATA && algo != DT_ALGO_SPECULATIVE)
+        return fail(DT_ERR_INVALID_ARG, "unknown algo");
+    if (out_kind != DT_OUT_CLASS_U8 && out_kind != DT_OUT_CLASS_I32 && out_kind != DT_OUT_LEAF_I32)
+        return fail(DT_ERR_INVALID_ARG, "unknown out_kind");
+    if (ld < t->n_features) return fail(DT_ERR_INVALID_ARG, "ld must be >= n_features");
+    const int mode = load_mode_for(d_x, ld, t->n_features, t->row_stride);
+    const Plan &plan = t->plan[algo][mode][out_kind == DT_OUT_CLASS_U8 ? 0 : 1];
+    if (plan.status != DT_OK) return fail(plan.status, plan.why);
+    info->waves_per_workgroup = plan.waves;
+    info->workgroups_per_cu = plan.blocks_per_cu;
+    info->lds_bytes = plan.lds_bytes;
+    info->result_buffer_tiles = plan.out_cap;
+    info->tables_in_lds = plan.tables_in_lds;
+    info->load_mode = mode;
+    return DT_OK;
+}
 
 dt_status dt_classify(const dt_tree *t, const float *d_x, int64_t n, int64_t ld, void *d_out,
                       dt_output out_kind, dt_algo algo, void *stream) {

@@ -107,6 +107,7 @@ void build_windows(const dt_node *nodes, const TreeShape &shape, int depth, Wind
         std::fill(slot_node.begin(), slot_node.end(), -1);
         slot_node[0] = roots[w];
         const size_t base = w * size_t(S);
+        // h is the 0-based heap index of the working array (stored at slot h + 1).
         // Unreachable exits end the walk like any leaf would; they stay -1.
         for (int32_t h = 0; h < S - 1; ++h) {
             const int32_t n = slot_node[size_t(h)];
@@ -119,8 +120,9 @@ void build_windows(const dt_node *nodes, const TreeShape &shape, int depth, Wind
                 out->exit_leaf[base + size_t(e)] = -(n + 1);
                 continue;
             }
-            out->feature[base + size_t(h)] = nodes[n].feature;
-            out->threshold[base + size_t(h)] = nodes[n].threshold;
+            // 1-based heap storage: heap node h lives in slot h + 1 (children 2p, 2p+1)
+            out->feature[base + size_t(h) + 1] = nodes[n].feature;
+            out->threshold[base + size_t(h) + 1] = nodes[n].threshold;
             for (int32_t b = 0; b < 2; ++b) {
                 const int32_t c = nodes[n].left + b;
                 const int32_t hc = 2 * h + 1 + b;
@@ -141,7 +143,7 @@ void build_windows(const dt_node *nodes, const TreeShape &shape, int depth, Wind
             }
         }
         // A root that is itself a leaf (single-node tree) is handled by the loop above:
-        // slot 0 holds the leaf and its always-right exit is the last one.
+        // heap node 0 (slot 1) holds the leaf and its always-right exit is the last one.
     }
 }
 

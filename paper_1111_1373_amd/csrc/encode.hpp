@@ -1,7 +1,9 @@
 // Host-side tree validation and window encoding shared by both GPU decompositions.
 //
 // A window is a block of at most D levels of the tree, rooted at a decision node and
-// embedded in a complete binary heap of 2^D - 1 slots (slot h has children 2h+1, 2h+2).
+// embedded in a complete binary heap stored 1-based: slot p in [1, 2^D) holds heap node p
+// (children 2p and 2p+1, so the two children of a node are one aligned 16-byte pair), and
+// slot 0 is padding.  Leaving the window at bottom position 2^D + e is exit e.
 // This is the "window" of Section 6 of the paper (evaluate a few levels, then continue
 // from the node reached), and it gives the speculative decomposition its fixed lane map
 // (the processor-node map of Procedure 5): lane h of a record's lane group evaluates

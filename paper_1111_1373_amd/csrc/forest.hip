@@ -46,11 +46,14 @@ __device__ __forceinline__ int majority(const uint32_t (&votes)[NV], int n_class
     return best;
 }
 
+// Trees walked together per lane by the data decomposition.
+constexpr int kIlp = 4;
+
 // SD = 0: data decomposition; SD > 0: speculative decomposition with window depth SD.
-template <int RS, bool VEC, bool TAB_LDS, int NV, int SD>
+template <int RS, int LOAD, bool TAB_LDS, int NV, int SD>
 __global__ void __launch_bounds__(512) forest_kernel(FArgs a) {
     extern __shared__ int4 lds[];
-    constexpr bool kPrefetch = VEC && RS <= 64;
+    constexpr bool kPrefetch = LOAD != kLoadScalar && RS <= 32;   // compute-bound: wide rows unprefetched
     const int wave = threadIdx.x >> 6;
     const int lane = threadIdx.x & 63;
     float *tile = reinterpret_cast<float *>(lds) + wave * (kTileRows * RS);
@@ -72,26 +75,28 @@ __global__ void __launch_bounds__(512) forest_kernel(FArgs a) {
         }
     };
 
+    // Full tiles are prefetched one group ahead; the partial last tile is staged directly.
+    const int64_t n_full = a.in.n / kTileRows;
     int64_t g = blockIdx.x;
-    dev::VecTile<(kPrefetch ? RS : 4)> buf;
+    dev::VecTile<(kPrefetch ? RS : 4), LOAD == kLoadExact> buf;
     if constexpr (kPrefetch) {
         const int64_t t0 = g * a.waves + wave;
-        if (g < n_groups && t0 < a.in.n_tiles) buf.load(a.in, t0, lane);
+        if (g < n_groups && t0 < n_full) buf.load_full(a.in, t0, lane);
     }
     for (; g < n_groups; g += gridDim.x) {
         const int64_t t = g * a.waves + wave;
         const bool active = t < a.in.n_tiles;        // uniform per wavefront
         dev::wave_sync();
         if (active) {
-            if constexpr (kPrefetch)
+            if (kPrefetch && t < n_full)
                 buf.store(a.in, tile, lane);
             else
-                dev::stage_now<RS, VEC>(a.in, tile, t, lane);
+                dev::stage_now<RS, LOAD>(a.in, tile, t, lane);
         }
         dev::wave_sync();
         if constexpr (kPrefetch) {
             const int64_t tn = t + int64_t(gridDim.x) * a.waves;
-            if (tn < a.in.n_tiles) buf.load(a.in, tn, lane);
+            if (tn < n_full) buf.load_full(a.in, tn, lane);
         }
 
         uint32_t votes[NV];
@@ -106,7 +111,25 @@ __global__ void __launch_bounds__(512) forest_kernel(FArgs a) {
                 __syncthreads();
                 if (active) {
                     const char *cbase = reinterpret_cast<const char *>(tab);
-                    for (int k = ch.x; k < ch.y; ++k) {
+                    int k = ch.x;
+                    if constexpr (SD == 0) {
+                        for (; k + kIlp <= ch.y; k += kIlp) {
+                            const char *base[kIlp];
+                            int sb[kIlp], lv[kIlp];
+                            int32_t code[kIlp];
+#pragma unroll
+                            for (int i = 0; i < kIlp; ++i) {
+                                const int4 d = a.trees[k + i];
+                                base[i] = cbase + (d.x - ch.z);
+                                sb[i] = d.y;
+                                lv[i] = d.z;
+                            }
+                            dev::walk_data_k<kIlp>(base, sb, lv, a.depth, row, sw, code);
+#pragma unroll
+                            for (int i = 0; i < kIlp; ++i) add_vote(votes, ~code[i]);
+                        }
+                    }
+                    for (; k < ch.y; ++k) {
                         const int4 d = a.trees[k];   // {byte_off, slot_bytes, levels, 0}
                         add_vote(votes, ~eval_tree(cbase + (d.x - ch.z), d.z, d.y));
                     }
@@ -114,7 +137,25 @@ __global__ void __launch_bounds__(512) forest_kernel(FArgs a) {
             } else {
                 if (active) {
                     const char *gbase = reinterpret_cast<const char *>(a.tables);
-                    for (int k = ch.x; k < ch.y; ++k) {
+                    int k = ch.x;
+                    if constexpr (SD == 0) {
+                        for (; k + kIlp <= ch.y; k += kIlp) {
+                            const char *base[kIlp];
+                            int sb[kIlp], lv[kIlp];
+                            int32_t code[kIlp];
+#pragma unroll
+                            for (int i = 0; i < kIlp; ++i) {
+                                const int4 d = a.trees[k + i];
+                                base[i] = gbase + d.x;
+                                sb[i] = d.y;
+                                lv[i] = d.z;
+                            }
+                            dev::walk_data_k<kIlp>(base, sb, lv, a.depth, row, sw, code);
+#pragma unroll
+                            for (int i = 0; i < kIlp; ++i) add_vote(votes, ~code[i]);
+                        }
+                    }
+                    for (; k < ch.y; ++k) {
                         const int4 d = a.trees[k];
                         add_vote(votes, ~eval_tree(gbase + d.x, d.z, d.y));
                     }
@@ -127,46 +168,53 @@ __global__ void __launch_bounds__(512) forest_kernel(FArgs a) {
     }
 }
 
-template <int RS, bool VEC, bool TAB_LDS, int NV>
+template <int RS, int LOAD, bool TAB_LDS, int NV>
 const void *for_votes(int algo, int depth) {
     if (algo == kAlgoData)
-        return reinterpret_cast<const void *>(&forest_kernel<RS, VEC, TAB_LDS, NV, 0>);
+        return reinterpret_cast<const void *>(&forest_kernel<RS, LOAD, TAB_LDS, NV, 0>);
     if (depth == 4)
-        return reinterpret_cast<const void *>(&forest_kernel<RS, VEC, TAB_LDS, NV, 4>);
+        return reinterpret_cast<const void *>(&forest_kernel<RS, LOAD, TAB_LDS, NV, 4>);
     return nullptr;
 }
 
-template <int RS, bool VEC, bool TAB_LDS>
+template <int RS, int LOAD, bool TAB_LDS>
 const void *for_tab(int algo, int vote_words, int depth) {
     switch (vote_words) {
-        case 2: return for_votes<RS, VEC, TAB_LDS, 2>(algo, depth);
-        case 4: return for_votes<RS, VEC, TAB_LDS, 4>(algo, depth);
-        case 16: return for_votes<RS, VEC, TAB_LDS, 16>(algo, depth);
+        case 2: return for_votes<RS, LOAD, TAB_LDS, 2>(algo, depth);
+        case 4: return for_votes<RS, LOAD, TAB_LDS, 4>(algo, depth);
+        case 16: return for_votes<RS, LOAD, TAB_LDS, 16>(algo, depth);
         default: return nullptr;
     }
 }
 
+template <int RS, int LOAD>
+const void *for_load(int algo, bool tab_lds, int vote_words, int depth) {
+    return tab_lds ? for_tab<RS, LOAD, true>(algo, vote_words, depth)
+                   : for_tab<RS, LOAD, false>(algo, vote_words, depth);
+}
+
 template <int RS>
-const void *for_stride(int algo, bool vec, bool tab_lds, int vote_words, int depth) {
-    if (vec)
-        return tab_lds ? for_tab<RS, true, true>(algo, vote_words, depth)
-                       : for_tab<RS, true, false>(algo, vote_words, depth);
-    return tab_lds ? for_tab<RS, false, true>(algo, vote_words, depth)
-                   : for_tab<RS, false, false>(algo, vote_words, depth);
+const void *for_stride(int algo, int load_mode, bool tab_lds, int vote_words, int depth) {
+    switch (load_mode) {
+        case kLoadScalar: return for_load<RS, kLoadScalar>(algo, tab_lds, vote_words, depth);
+        case kLoadVec: return for_load<RS, kLoadVec>(algo, tab_lds, vote_words, depth);
+        case kLoadExact: return for_load<RS, kLoadExact>(algo, tab_lds, vote_words, depth);
+        default: return nullptr;
+    }
 }
 
 }  // namespace
 
-const void *forest_kernel_for(int algo, int row_stride, bool vec, bool tables_in_lds,
+const void *forest_kernel_for(int algo, int row_stride, int load_mode, bool tables_in_lds,
                               int vote_words, int depth) {
     switch (row_stride) {
-        case 4: return for_stride<4>(algo, vec, tables_in_lds, vote_words, depth);
-        case 8: return for_stride<8>(algo, vec, tables_in_lds, vote_words, depth);
-        case 16: return for_stride<16>(algo, vec, tables_in_lds, vote_words, depth);
-        case 32: return for_stride<32>(algo, vec, tables_in_lds, vote_words, depth);
-        case 64: return for_stride<64>(algo, vec, tables_in_lds, vote_words, depth);
-        case 128: return for_stride<128>(algo, vec, tables_in_lds, vote_words, depth);
-        case 256: return for_stride<256>(algo, vec, tables_in_lds, vote_words, depth);
+        case 4: return for_stride<4>(algo, load_mode, tables_in_lds, vote_words, depth);
+        case 8: return for_stride<8>(algo, load_mode, tables_in_lds, vote_words, depth);
+        case 16: return for_stride<16>(algo, load_mode, tables_in_lds, vote_words, depth);
+        case 32: return for_stride<32>(algo, load_mode, tables_in_lds, vote_words, depth);
+        case 64: return for_stride<64>(algo, load_mode, tables_in_lds, vote_words, depth);
+        case 128: return for_stride<128>(algo, load_mode, tables_in_lds, vote_words, depth);
+        case 256: return for_stride<256>(algo, load_mode, tables_in_lds, vote_words, depth);
         default: return nullptr;
     }
 }

@@ -34,8 +34,13 @@ struct KArgs {
     int32_t levels;          // windows on the longest path
     int32_t waves;           // wavefronts per workgroup
     int32_t out_kind;        // 0: uint8 output, 1: int32 output
+    int32_t out_cap;         // tiles of results each wavefront buffers in the LDS (>= 1)
+    int32_t out_vec;         // 1: `out` is 16-byte aligned (flushes use 16-byte stores)
     void *out;
 };
+
+// LDS bytes of one wavefront's result buffer: cap tiles of 64 results of out_bytes each.
+__host__ __device__ inline int out_buffer_bytes(int cap, int out_bytes) { return cap * kTileRows * out_bytes; }
 
 // Forest kernel arguments.  Tree k's tables are the bytes [off_k, off_k + slot_bytes_k)
 // (slots) followed by its exit codes, inside `tables`; trees[k] = {off_k, slot_bytes_k,
@@ -58,14 +63,23 @@ struct FArgs {
 
 enum KernelAlgo { kAlgoData = 0, kAlgoSpec = 1 };
 
-// Kernel instance for (algorithm, LDS row stride, vectorised loads, tables staged in the
-// LDS or read from global memory, window depth), or nullptr if no such instance exists.
+// How record tiles are read from HBM.
+enum LoadMode {
+    kLoadScalar = 0,   // any ld >= F, 4-byte aligned: one float per load
+    kLoadVec = 1,      // ld == F, F % 4 == 0, 16-byte aligned base: 16-byte loads
+    kLoadExact = 2,    // as kLoadVec and F == the LDS row stride: every lane loads RS/4
+                       // vectors per tile with no bounds test
+    kLoadModes = 3
+};
+
+// Kernel instance for (algorithm, LDS row stride, load mode, tables staged in the LDS or
+// read from global memory, window depth), or nullptr if no such instance exists.
 // `depth` is ignored by the data kernel.
-const void *kernel_for(int algo, int row_stride, bool vec, bool tables_in_lds, int depth);
+const void *kernel_for(int algo, int row_stride, int load_mode, bool tables_in_lds, int depth);
 
 // Forest kernel instance; `vote_words` = 32-bit words of packed 8-bit counters
-// (1, 2, 4, 8 or 16 for up to 4, 8, 16, 32 or 64 classes).
-const void *forest_kernel_for(int algo, int row_stride, bool vec, bool tables_in_lds,
+// (2, 4 or 16 for up to 8, 16 or 64 classes).
+const void *forest_kernel_for(int algo, int row_stride, int load_mode, bool tables_in_lds,
                               int vote_words, int depth);
 
 // One-time per-instance setup (raise the dynamic LDS limit to the device maximum).
@@ -77,9 +91,10 @@ hipError_t launch_kernel(const void *fn, const KArgs &args, int blocks, int lds_
 hipError_t launch_forest(const void *fn, const FArgs &args, int blocks, int lds_bytes,
                          hipStream_t stream);
 
-// Dynamic LDS a workgroup of `waves` wavefronts needs.
-inline int lds_bytes_for(int table_bytes, int row_stride, int waves) {
-    return table_bytes + waves * kTileRows * row_stride * 4;
+// Dynamic LDS of a workgroup of `waves` wavefronts: tables, one record tile per wavefront,
+// then (single-tree kernels) one result buffer of `out_bytes_per_wave` per wavefront.
+inline int lds_bytes_for(int table_bytes, int row_stride, int waves, int out_bytes_per_wave = 0) {
+    return table_bytes + waves * (kTileRows * row_stride * 4 + out_bytes_per_wave);
 }
 
 }  // namespace dtree

@@ -37,7 +37,8 @@ NODE_DTYPE = np.dtype(
 
 
 class TreeOptions(ctypes.Structure):
-    _fields_ = [("data_window_depth", ctypes.c_int32), ("spec_window_depth", ctypes.c_int32)]
+    _fields_ = [("data_window_depth", ctypes.c_int32), ("spec_window_depth", ctypes.c_int32),
+                ("waves_per_cu", ctypes.c_int32)]
 
 
 class TreeInfo(ctypes.Structure):
@@ -46,6 +47,15 @@ class TreeInfo(ctypes.Structure):
         "data_window_depth", "data_windows", "data_levels",
         "spec_window_depth", "spec_windows", "spec_levels")] + [
         ("data_table_bytes", ctypes.c_int64), ("spec_table_bytes", ctypes.c_int64)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
+class LaunchInfo(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "waves_per_workgroup", "workgroups_per_cu", "lds_bytes", "result_buffer_tiles",
+        "tables_in_lds", "load_mode")]
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}
@@ -61,6 +71,7 @@ _PROTOS = {
     "dt_tree_create": (ctypes.c_int, [_p, _i32, _i32, _i32, _p, _p]),
     "dt_tree_get_info": (ctypes.c_int, [_p, _p]),
     "dt_tree_destroy": (None, [_p]),
+    "dt_tree_launch_info": (ctypes.c_int, [_p, _p, _i64, ctypes.c_int, ctypes.c_int, _p]),
     "dt_classify": (ctypes.c_int, [_p, _p, _i64, _i64, _p, ctypes.c_int, ctypes.c_int, _p]),
     "dt_forest_create": (ctypes.c_int, [_p, _p, _i32, _i32, _i32, _p, _p]),
     "dt_forest_destroy": (None, [_p]),
@@ -94,16 +105,16 @@ def _nodes(nodes) -> np.ndarray:
     return arr
 
 
-def _options(data_window_depth: int, spec_window_depth: int) -> TreeOptions:
-    return TreeOptions(int(data_window_depth), int(spec_window_depth))
+def _options(data_window_depth: int, spec_window_depth: int, waves_per_cu: int = 0) -> TreeOptions:
+    return TreeOptions(int(data_window_depth), int(spec_window_depth), int(waves_per_cu))
 
 
 def tree_check(nodes, n_features: int, n_classes: int, data_window_depth: int = 0,
-               spec_window_depth: int = 0) -> dict:
+               spec_window_depth: int = 0, waves_per_cu: int = 0) -> dict:
     """Validate a tree on the host and describe its encodings (no GPU needed)."""
     nd = _nodes(nodes)
     info = TreeInfo()
-    opt = _options(data_window_depth, spec_window_depth)
+    opt = _options(data_window_depth, spec_window_depth, waves_per_cu)
     _check(_lib.dt_tree_check(nd.ctypes.data, len(nd), n_features, n_classes,
                               ctypes.byref(opt), ctypes.byref(info)), "dt_tree_check")
     return info.as_dict()
@@ -165,12 +176,12 @@ class Tree:
     """A tree uploaded to the current device (``dt_tree_create``)."""
 
     def __init__(self, nodes, n_features: int, n_classes: int, data_window_depth: int = 0,
-                 spec_window_depth: int = 0):
+                 spec_window_depth: int = 0, waves_per_cu: int = 0):
         nd = _nodes(nodes)
         self.n_features = int(n_features)
         self.n_classes = int(n_classes)
         self._h = ctypes.c_void_p()
-        opt = _options(data_window_depth, spec_window_depth)
+        opt = _options(data_window_depth, spec_window_depth, waves_per_cu)
         _check(_lib.dt_tree_create(nd.ctypes.data, len(nd), n_features, n_classes,
                                    ctypes.byref(opt), ctypes.byref(self._h)), "dt_tree_create")
 
@@ -178,6 +189,14 @@ class Tree:
     def info(self) -> dict:
         info = TreeInfo()
         _check(_lib.dt_tree_get_info(self._h, ctypes.byref(info)), "dt_tree_get_info")
+        return info.as_dict()
+
+    def launch_info(self, x, algo: str = "data", out_kind: str = "class_u8") -> dict:
+        """Launch shape classify() uses for ``x`` (diagnostic)."""
+        ptr, _, ld = _features_arg(x, self.n_features)
+        info = LaunchInfo()
+        _check(_lib.dt_tree_launch_info(self._h, ptr, ld, OUT_KINDS[out_kind], ALGOS[algo],
+                                        ctypes.byref(info)), "dt_tree_launch_info")
         return info.as_dict()
 
     def classify(self, x, algo: str = "data", out_kind: str = "class_u8", out=None, stream=None):
@@ -206,13 +225,13 @@ class Forest:
     """A forest uploaded to the current device (``dt_forest_create``)."""
 
     def __init__(self, nodes, tree_offsets, n_features: int, n_classes: int,
-                 data_window_depth: int = 0, spec_window_depth: int = 0):
+                 data_window_depth: int = 0, spec_window_depth: int = 0, waves_per_cu: int = 0):
         nd = _nodes(nodes)
         off = np.ascontiguousarray(tree_offsets, dtype=np.int32)
         self.n_features = int(n_features)
         self.n_classes = int(n_classes)
         self._h = ctypes.c_void_p()
-        opt = _options(data_window_depth, spec_window_depth)
+        opt = _options(data_window_depth, spec_window_depth, waves_per_cu)
         _check(_lib.dt_forest_create(nd.ctypes.data, off.ctypes.data, len(off) - 1, n_features,
                                      n_classes, ctypes.byref(opt), ctypes.byref(self._h)),
                "dt_forest_create")

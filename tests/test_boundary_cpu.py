@@ -152,7 +152,8 @@ def test_non_bfs_order_accepted():
 # ----------------------------------------------------------------------- window encoding
 
 def walk_tables_heap(tab, x, exits_key="exit_class"):
-    """Data-decomposition form: per record, D heap steps per window, then the exit."""
+    """Data-decomposition form: per record, D steps p <- 2p + !(x[f_p] < t_p) down the
+    1-based heap of each window (root slot 1), then the exit at position p - 2^D."""
     D = tab["depth"]
     S = 1 << D
     n = x.shape[0]
@@ -161,12 +162,12 @@ def walk_tables_heap(tab, x, exits_key="exit_class"):
     code = np.full(n, 0, dtype=np.int64)
     done = np.zeros(n, dtype=bool)
     for _ in range(tab["levels"]):
-        h = np.zeros(n, dtype=np.int64)
+        p = np.ones(n, dtype=np.int64)
         for _ in range(D):
-            f = tab["feature"][w, h]
-            t = tab["threshold"][w, h]
-            h = 2 * h + 1 + (~(x[rows, f] < t)).astype(np.int64)
-        c = tab[exits_key][w, h - (S - 1)].astype(np.int64)
+            f = tab["feature"][w, p]
+            t = tab["threshold"][w, p]
+            p = 2 * p + (~(x[rows, f] < t)).astype(np.int64)
+        c = tab[exits_key][w, p - S].astype(np.int64)
         code = np.where(done, code, c)
         done |= c < 0
         w = np.where(done, w, np.maximum(c, 0))
@@ -187,10 +188,10 @@ def walk_tables_mask(tab, x, exits_key="exit_class"):
         f = tab["feature"][w]                              # [n, S]
         t = tab["threshold"][w]
         bits = ~(x[rows[:, None], f] < t)                  # all slots at once
-        h = np.zeros(n, dtype=np.int64)
+        p = np.ones(n, dtype=np.int64)
         for _ in range(D):
-            h = 2 * h + 1 + bits[rows, h].astype(np.int64)
-        c = tab[exits_key][w, h - (S - 1)].astype(np.int64)
+            p = 2 * p + bits[rows, p].astype(np.int64)
+        c = tab[exits_key][w, p - S].astype(np.int64)
         code = np.where(done, code, c)
         done |= c < 0
         w = np.where(done, w, np.maximum(c, 0))
@@ -243,8 +244,9 @@ def test_complete_tree_window_counts(d, D):
     tab = dt.encode_windows(nodes, 4, 3, D)
     assert tab["n_windows"] == sum(1 << (m * D) for m in range(0, (d + D - 1) // D))
     assert tab["levels"] == -(-d // D)
-    # in a complete window every slot but the padding holds a decision node
-    assert np.isfinite(tab["threshold"][:, :-1]).all() or d % D != 0
+    # in a complete window every slot but the padding (slot 0) holds a decision node
+    assert np.isfinite(tab["threshold"][:, 1:]).all() or d % D != 0
+    assert np.isneginf(tab["threshold"][:, 0]).all()
 
 
 def test_default_depths_and_info():
