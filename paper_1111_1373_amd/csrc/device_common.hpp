@@ -233,6 +233,8 @@ template <int K>
 __device__ __forceinline__ void walk_data_k(const char *const (&base)[K], const int (&slot_bytes)[K],
                                             const int (&levels)[K], int D, const float *row,
                                             int sw, int32_t (&code)[K]) {
+    // K independent chains already hide the LDS latency, so each level reads just the
+    // node's own 8-byte slot (no lookahead): fewer LDS bytes and bank conflicts per step.
     const int S = 1 << D;
     int w[K];
     int max_levels = 0;
@@ -245,28 +247,22 @@ __device__ __forceinline__ void walk_data_k(const char *const (&base)[K], const 
     for (int level = 0; level < max_levels; ++level) {
         const Slot *win[K];
         int p[K];
-        Slot s[K];
 #pragma unroll
         for (int i = 0; i < K; ++i) {
             win[i] = reinterpret_cast<const Slot *>(base[i]) + (w[i] << D);
             p[i] = 1;
-            s[i] = win[i][1];
         }
-        for (int k = 1; k < D; ++k) {
+        for (int k = 0; k < D; ++k) {
 #pragma unroll
             for (int i = 0; i < K; ++i) {
-                const float xv = row[s[i].f ^ sw];
-                const Slot2 kids = *reinterpret_cast<const Slot2 *>(win[i] + 2 * p[i]);
-                const bool right = !(xv < s[i].t);
-                p[i] = 2 * p[i] + int(right);
-                s[i] = right ? kids.r : kids.l;
+                const Slot s = win[i][p[i]];
+                const float xv = row[s.f ^ sw];
+                p[i] = 2 * p[i] + int(!(xv < s.t));
             }
         }
         bool all_done = true;
 #pragma unroll
         for (int i = 0; i < K; ++i) {
-            const float xv = row[s[i].f ^ sw];
-            p[i] = 2 * p[i] + int(!(xv < s[i].t));
             if (code[i] >= 0 && level < levels[i]) {
                 const int32_t *ex = reinterpret_cast<const int32_t *>(base[i] + slot_bytes[i]);
                 const int32_t c = ex[(w[i] << D) + p[i] - S];
