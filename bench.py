@@ -34,9 +34,15 @@ PAPER_CONTEXT = {"speculative_us": 404.466, "data_us": 538.235, "ratio": 404.466
                  "workload": "65,536 records x 19 attributes, 31-node tree"}
 
 
-def kernel_source_hash() -> str:
+KERNEL_SOURCES = {"data": "kernels.hip", "speculative": "kernels.hip", "path": "path.hip",
+                  "forest": "forest.hip"}
+
+
+def kernel_source_hash(algo: str) -> str:
+    """Hash of the sources that decide what the kernel of `algo` ("data", "speculative",
+    "path" or "forest") does and how it is launched."""
     h = hashlib.sha256()
-    for f in ("kernels.hip", "kernels.hpp", "forest.hip", "device_common.hpp", "dtree.hip",
+    for f in (KERNEL_SOURCES[algo], "kernels.hpp", "device_common.hpp", "dtree.hip",
               "encode.cpp", "encode.hpp"):
         with open(os.path.join(ROOT, "paper_1111_1373_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
@@ -54,7 +60,7 @@ def recorded_traffic(workload: str, algo: str):
         if "=" in line and not line.lstrip().startswith("#"):
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
-    if kv.get("source_hash") != kernel_source_hash():
+    if kv.get("source_hash") != kernel_source_hash("forest" if workload == "C5" else algo):
         return None
     try:
         return float(kv["hbm_bytes_per_launch"])
@@ -68,7 +74,9 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=4, choices=[1, 2, 3, 4, 5])
-    ap.add_argument("--algos", default="data,speculative")
+    ap.add_argument("--algos", default="auto",
+                    help="comma-separated decompositions (data, speculative, path); auto: "
+                         "all that the workload supports")
     ap.add_argument("--spec-window-depth", type=int, default=0)
     ap.add_argument("--data-window-depth", type=int, default=0)
     ap.add_argument("--waves-per-cu", type=int, default=0)
@@ -136,11 +144,15 @@ def main() -> int:
                          % (n, w.name, len(t_or))}
     log("oracle passes", len(t_or), "mean s", sum(t_or) / len(t_or))
 
+    algos = args.algos.split(",")
+    if args.algos == "auto":
+        algos = ["data", "speculative"] if w.is_forest else ["data", "speculative", "path"]
+
     stream = torch.cuda.current_stream()
     feature_bytes = n * F * 4
     algo_bytes = feature_bytes + n * 1          # fp32 features read + uint8 labels written
     results = {}
-    for algo in args.algos.split(","):
+    for algo in algos:
         out = torch.empty(n, dtype=torch.uint8, device="cuda")
         for _ in range(args.warmup):
             tree.classify(x, algo=algo, out=out, stream=stream)
@@ -169,6 +181,9 @@ def main() -> int:
             "feature_frac_of_peak": feature_bytes / kavg / 1e9 / PEAK_HBM_GBPS,
             "mismatches_vs_oracle": mism,
             "window_depth": info["data_window_depth" if algo == "data" else "spec_window_depth"],
+            "kernel": ("forest_kernel(%s)" % algo) if w.is_forest
+                      else {"data": "data_kernel", "speculative": "spec_kernel",
+                            "path": "path_kernel"}[algo],
         }
         if w.is_forest:
             results[algo]["tree_samples_per_s"] = results[algo]["samples_per_s"] * info["n_trees"]
@@ -203,8 +218,7 @@ def main() -> int:
                      "frac": achieved / PEAK_HBM_GBPS,
                      "traffic": traffic,
                      "algorithmic_bytes_per_launch": algo_bytes,
-                     "kernel": ("forest_kernel(%s)" % best) if w.is_forest
-                               else "%s_kernel" % ("data" if best == "data" else "spec")},
+                     "kernel": r["kernel"]},
         "cpu_baseline": cpu,
         "parity": "bit-exact vs oracle on all %d records" % n
                   if all(v["mismatches_vs_oracle"] == 0 for v in results.values())
@@ -213,8 +227,11 @@ def main() -> int:
         "speculative_over_data_kernel_time": (
             results["speculative"]["kernel_us"]["avg"] / results["data"]["kernel_us"]["avg"]
             if "speculative" in results and "data" in results else None),
+        "path_over_speculative_kernel_time": (
+            results["path"]["kernel_us"]["avg"] / results["speculative"]["kernel_us"]["avg"]
+            if "path" in results and "speculative" in results else None),
         "paper_context": PAPER_CONTEXT,
-        "source_hash": kernel_source_hash(),
+        "source_hash": kernel_source_hash("forest" if w.is_forest else best),
     }
     print(json.dumps(line), flush=True)
     return 0 if line["parity"] != "MISMATCH" else 1

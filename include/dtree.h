@@ -12,6 +12,9 @@
  *     64-bit wavefront mask, and the reached node is found by walking the mask.  Trees
  *     deeper than one block are evaluated block after block (the "window" of
  *     Section 6).
+ *   - DT_ALGO_PATH: the same speculative evaluation, reduced as Procedure 5 prints it:
+ *     a path array in the LDS, leaves pointing to themselves, pointer jumping until the
+ *     root's entry names a leaf.  Kept to compare the paper's mechanism with the mask.
  *   - Forests (Section 1, trees evaluated one after another and combined): majority
  *     vote, ties to the smallest class id.
  *
@@ -42,7 +45,7 @@
 extern "C" {
 #endif
 
-#define DT_ABI_VERSION 1
+#define DT_ABI_VERSION 2
 
 typedef enum {
     DT_OK = 0,
@@ -56,7 +59,9 @@ typedef enum {
 
 typedef enum {
     DT_ALGO_DATA = 0,         /* one lane per record (Procedure 3)                          */
-    DT_ALGO_SPECULATIVE = 1   /* lanes per decision node, predicate mask walk (Proc. 4-5)  */
+    DT_ALGO_SPECULATIVE = 1,  /* lanes per decision node, predicate mask walk (Proc. 4-5)  */
+    DT_ALGO_PATH = 2          /* lanes per decision node, path array reduced by pointer
+                                 jumping as printed in Procedure 5 (single trees only)      */
 } dt_algo;
 
 typedef enum {
@@ -94,6 +99,9 @@ typedef struct {
     int32_t waves_per_cu;      /* launch tuning: resident wavefronts per compute unit
                                   (0 = the library's choice, about 64 KiB of record tiles in
                                   flight per CU); limited by the LDS and registers */
+    int32_t path_hops;         /* DT_ALGO_PATH: entries read further along per reduction
+                                  round, 1..8 (0 = 2: path[i] <- path[path[path[i]]], the
+                                  form printed in Procedure 5) */
 } dt_tree_options;
 
 /* Shape of a tree and of its two encodings. */

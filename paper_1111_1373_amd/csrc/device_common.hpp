@@ -347,6 +347,128 @@ struct Spec {
     }
 };
 
+// ---- single-tree kernel scaffolding ------------------------------------------------------
+
+// Window tables: staged into the LDS once per workgroup (TAB_LDS), or read in place from
+// global memory.  Returns the first LDS byte after the tables (where record tiles start).
+template <bool TAB_LDS>
+__device__ __forceinline__ char *bind_tables(const KArgs &a, int4 *lds, const Slot *&slots,
+                                             const int32_t *&exits) {
+    if constexpr (TAB_LDS) {
+        const int ns = a.slot_bytes >> 4;
+        const int ne = a.exit_bytes >> 4;
+        for (int i = threadIdx.x; i < ns; i += blockDim.x) lds[i] = a.slots[i];
+        for (int i = threadIdx.x; i < ne; i += blockDim.x) lds[ns + i] = a.exits[i];
+        __syncthreads();
+        slots = reinterpret_cast<const Slot *>(lds);
+        exits = reinterpret_cast<const int32_t *>(reinterpret_cast<const char *>(lds) + a.slot_bytes);
+        return reinterpret_cast<char *>(lds) + a.slot_bytes + a.exit_bytes;
+    } else {
+        slots = reinterpret_cast<const Slot *>(a.slots);
+        exits = reinterpret_cast<const int32_t *>(a.exits);
+        return reinterpret_cast<char *>(lds);
+    }
+}
+
+// Results of up to out_cap tiles are collected in the wavefront's LDS buffer and written in
+// bursts.  Writing each tile's 64 results as soon as they are known interleaves small
+// writes with the input stream, which measurably slows the stream; bursts of whole
+// 16-byte vectors do not.  buf holds results of records r0 .. r0 + count - 1.
+__device__ __forceinline__ void flush_results(const KArgs &a, const uint8_t *buf, int64_t r0,
+                                              int64_t r_end, int lane) {
+    const int esize = a.out_kind == 0 ? 1 : 4;
+    const int64_t r1 = r_end < a.in.n ? r_end : a.in.n;
+    const int nbytes = int(r1 - r0) * esize;
+    uint8_t *dst = static_cast<uint8_t *>(a.out) + r0 * esize;
+    int done = 0;
+    if (a.out_vec) {   // dst is 16-byte aligned: r0 is a multiple of 64 records
+        typedef int i32x4 __attribute__((ext_vector_type(4)));
+        const int nvec = nbytes >> 4;
+        for (int i = lane; i < nvec; i += 64)
+            __builtin_nontemporal_store(reinterpret_cast<const i32x4 *>(buf)[i],
+                                        reinterpret_cast<i32x4 *>(dst) + i);
+        done = nvec << 4;
+    }
+    if (esize == 1) {
+        for (int i = done + lane; i < nbytes; i += 64) dst[i] = buf[i];
+    } else {
+        for (int i = (done >> 2) + lane; i < (nbytes >> 2); i += 64)
+            reinterpret_cast<int32_t *>(dst)[i] = reinterpret_cast<const int32_t *>(buf)[i];
+    }
+}
+
+// Persistent tile loop.  Wavefront g of G takes the contiguous tile range
+// [g*chunk, (g+1)*chunk), chunk = ceil(tiles / G), so its results form one contiguous run
+// of the output.  `body(t)` walks staged tile t and returns each lane's result.  No
+// workgroup barrier inside: the wavefronts of a workgroup process different numbers of
+// tiles.
+template <int RS, int LOAD, class Body>
+__device__ __forceinline__ void tile_loop(const KArgs &a, float *tile, uint8_t *obuf, int lane,
+                                          Body body) {
+    const int64_t G = int64_t(gridDim.x) * a.waves;
+    const int64_t gw = int64_t(blockIdx.x) * a.waves + (threadIdx.x >> 6);
+    const int64_t chunk = (a.in.n_tiles + G - 1) / G;
+    const int64_t t0 = gw * chunk < a.in.n_tiles ? gw * chunk : a.in.n_tiles;
+    const int64_t t1 = t0 + chunk < a.in.n_tiles ? t0 + chunk : a.in.n_tiles;
+    const int64_t n_full = a.in.n / kTileRows;     // tiles with 64 valid records
+    const int esize = a.out_kind == 0 ? 1 : 4;
+    int64_t fl = t0;                               // first tile whose results are buffered
+
+    auto finish = [&](int64_t t, int32_t v) {
+        const int slot = int(t - fl) * kTileRows + lane;
+        if (esize == 1)
+            obuf[slot] = uint8_t(v);
+        else
+            reinterpret_cast<int32_t *>(obuf)[slot] = v;
+        if (t - fl == a.out_cap - 1 || t + 1 == t1) {
+            wave_sync();
+            flush_results(a, obuf, fl * kTileRows, (t + 1) * kTileRows, lane);
+            wave_sync();
+            fl = t + 1;
+        }
+    };
+
+    if constexpr (LOAD != kLoadScalar && RS <= 64) {
+        // Full tiles: the loads of tile t + 1 are in flight in registers while tile t is
+        // walked.  The partial last tile of the input, if any, is staged on its own.
+        VecTile<RS, LOAD == kLoadExact> buf;
+        const int64_t tf = t1 < n_full ? t1 : n_full;
+        int64_t t = t0;
+        if (t < tf) buf.load_full(a.in, t, lane);
+        for (; t < tf; ++t) {
+            wave_sync();                 // previous tile fully read
+            buf.store(a.in, tile, lane);
+            wave_sync();                 // tile visible to every lane
+            if (t + 1 < tf) buf.load_full(a.in, t + 1, lane);
+            finish(t, body(t));
+        }
+        if (t < t1) {                         // t == n_full: the partial tile
+            wave_sync();
+            stage_now<RS, LOAD>(a.in, tile, t, lane);
+            wave_sync();
+            finish(t, body(t));
+        }
+    } else {
+        for (int64_t t = t0; t < t1; ++t) {
+            wave_sync();
+            stage_now<RS, LOAD>(a.in, tile, t, lane);
+            wave_sync();
+            finish(t, body(t));
+        }
+    }
+}
+
+// LDS layout: [tables (if staged)] [one record tile per wavefront] [one result buffer per
+// wavefront].
+template <int RS>
+__device__ __forceinline__ void wave_buffers(const KArgs &a, char *after_tables, float *&tile,
+                                             uint8_t *&obuf) {
+    const int wave = threadIdx.x >> 6;
+    tile = reinterpret_cast<float *>(after_tables) + wave * (kTileRows * RS);
+    const int obytes = out_buffer_bytes(a.out_cap, a.out_kind == 0 ? 1 : 4);
+    obuf = reinterpret_cast<uint8_t *>(after_tables) + a.waves * (kTileRows * RS * 4) + wave * obytes;
+}
+
 template <class T>
 __device__ __forceinline__ void store_value(void *out, int out_kind, int64_t n, int64_t row,
                                             T v) {

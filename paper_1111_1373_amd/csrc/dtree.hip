@@ -102,6 +102,11 @@ void free_encoding(Encoding *enc) {
     enc->d_mem = nullptr;
 }
 
+// Pointer-jumping reach per round of the path kernel: entry <- the entry `hops` further
+// along.  Procedure 5 reads two further (path[path[path[i]]]).
+constexpr int kDefaultPathHops = 2;
+constexpr int kMaxPathHops = 8;
+
 dt_status check_options(const dt_tree_options *opt) {
     if (!opt) return DT_OK;
     if (opt->data_window_depth < 0 || opt->data_window_depth > dtree::kMaxWindowDepth)
@@ -110,6 +115,8 @@ dt_status check_options(const dt_tree_options *opt) {
         return fail(DT_ERR_INVALID_ARG, "spec_window_depth must be 0 (auto) or 1..6");
     if (opt->waves_per_cu < 0 || opt->waves_per_cu > 32)
         return fail(DT_ERR_INVALID_ARG, "waves_per_cu must be 0 (auto) or 1..32");
+    if (opt->path_hops < 0 || opt->path_hops > kMaxPathHops)
+        return fail(DT_ERR_INVALID_ARG, "path_hops must be 0 (auto) or 1..8");
     return DT_OK;
 }
 
@@ -163,7 +170,7 @@ std::vector<const void *> g_prepared;
 // record, runs best with 8 wavefronts per CU on every tile width (fewer leave its LDS
 // latency exposed, more slow it down).
 int target_waves_per_cu(int algo, int row_stride) {
-    if (algo == DT_ALGO_SPECULATIVE) return 8;
+    if (algo != DT_ALGO_DATA) return 8;
     const int tile_bytes = dtree::kTileRows * row_stride * 4;
     return std::max(2, std::min(32, (64 * 1024) / tile_bytes));
 }
@@ -186,10 +193,12 @@ constexpr int kMinLdsWaves = 2;
 constexpr int kMaxOutCap = 256;
 
 // Single-tree plan: workgroup shape, resident workgroups per CU and the result buffer, for
-// results of `out_bytes` bytes (1 or 4).
+// results of `out_bytes` bytes (1 or 4).  The path kernel also keeps its path arrays
+// (kPathIntsPerWave ints per wavefront) after the result buffers.
 dt_status make_plan(const DeviceCaps &caps, int algo, int row_stride, int load_mode, int depth,
                     int64_t table_bytes, int out_bytes, int waves_per_cu, Plan *plan) {
-    const int tile_bytes = dtree::kTileRows * row_stride * 4;
+    const int path_bytes = algo == DT_ALGO_PATH ? dtree::kPathIntsPerWave * 4 : 0;
+    const int tile_bytes = dtree::kTileRows * row_stride * 4 + path_bytes;
     const int res_bytes = dtree::kTileRows * out_bytes;   // one tile of results
     if (tile_bytes + res_bytes > caps.lds_per_block) {
         plan->why = "one record tile exceeds the workgroup LDS";
@@ -219,7 +228,8 @@ dt_status make_plan(const DeviceCaps &caps, int algo, int row_stride, int load_m
             if (table_lds + w * (tile_bytes + res_bytes) > budget) continue;
             const int cap =
                 std::min(kMaxOutCap, (budget - table_lds - w * tile_bytes) / (w * res_bytes));
-            const int lds = dtree::lds_bytes_for(table_lds, row_stride, w, cap * res_bytes);
+            const int lds =
+                dtree::lds_bytes_for(table_lds, row_stride, w, cap * res_bytes) + w * path_bytes;
             int nb = 0;
             hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, plan->fn, w * 64,
                                                                         size_t(lds));
@@ -255,9 +265,17 @@ struct dt_tree {
     dtree::TreeShape shape;
     int32_t n_features = 0, n_classes = 0;
     int row_stride = 0;
-    Encoding enc[2];              // [DT_ALGO_DATA], [DT_ALGO_SPECULATIVE]
-    Plan plan[2][dtree::kLoadModes][2];   // [algo][load mode][uint8 / int32 results]
+    int path_hops = kDefaultPathHops;
+    Encoding enc[2];              // data windows, speculative windows (also the path kernel's)
+    Plan plan[3][dtree::kLoadModes][2];   // [algo][load mode][uint8 / int32 results]
 };
+
+// Encoding an algorithm runs on: the path kernel reduces the speculative windows.
+static inline int encoding_of(int algo) { return algo == DT_ALGO_DATA ? 0 : 1; }
+
+static bool single_tree_algo(dt_algo algo) {
+    return algo == DT_ALGO_DATA || algo == DT_ALGO_SPECULATIVE || algo == DT_ALGO_PATH;
+}
 
 namespace {
 
@@ -320,8 +338,7 @@ dt_status classify_impl(const dt_tree *tree, const float *d_x, int64_t n, int64_
                         void *d_out, dt_output out_kind, dt_algo algo, void *stream) {
     if (!tree) return fail(DT_ERR_INVALID_ARG, "tree is NULL");
     if (n < 0) return fail(DT_ERR_INVALID_ARG, "n must be >= 0");
-    if (algo != DT_ALGO_DATA && algo != DT_ALGO_SPECULATIVE)
-        return fail(DT_ERR_INVALID_ARG, "unknown algo");
+    if (!single_tree_algo(algo)) return fail(DT_ERR_INVALID_ARG, "unknown algo");
     if (out_kind != DT_OUT_CLASS_U8 && out_kind != DT_OUT_CLASS_I32 &&
         out_kind != DT_OUT_LEAF_I32)
         return fail(DT_ERR_INVALID_ARG, "unknown out_kind");
@@ -342,7 +359,7 @@ dt_status classify_impl(const dt_tree *tree, const float *d_x, int64_t n, int64_
     const Plan &plan = tree->plan[algo][load_mode_for(d_x, ld, tree->n_features, tree->row_stride)]
                                  [out_kind == DT_OUT_CLASS_U8 ? 0 : 1];
     if (plan.status != DT_OK) return fail(plan.status, plan.why);
-    const Encoding &enc = tree->enc[algo];
+    const Encoding &enc = tree->enc[encoding_of(algo)];
 
     dtree::KArgs a{};
     a.in = make_rows(d_x, n, ld, tree->n_features);
@@ -356,6 +373,7 @@ dt_status classify_impl(const dt_tree *tree, const float *d_x, int64_t n, int64_
     a.out_kind = out_kind == DT_OUT_CLASS_U8 ? 0 : 1;
     a.out_cap = plan.out_cap;
     a.out_vec = (reinterpret_cast<uintptr_t>(d_out) & 15u) == 0 ? 1 : 0;
+    a.hops = tree->path_hops;
     a.out = d_out;
     const int64_t want = (a.in.n_tiles + plan.waves - 1) / plan.waves;
     const int64_t resident = int64_t(plan.blocks_per_cu) * tree->caps.n_cu;
@@ -383,18 +401,22 @@ dt_status create_impl(const dt_node *nodes, int32_t n_nodes, int32_t n_features,
     t->n_features = n_features;
     t->n_classes = n_classes;
     t->row_stride = row_stride_for(n_features);
+    if (opt && opt->path_hops) t->path_hops = opt->path_hops;
     int depth[2];
     window_depths(nodes, shape, opt, &depth[0], &depth[1]);
-    for (int algo = 0; algo < 2; ++algo) {
+    for (int e = 0; e < 2; ++e) {
         dtree::WindowTables wt;
-        dtree::build_windows(nodes, shape, depth[algo], &wt);
-        st = upload_encoding(wt, &t->enc[algo]);
+        dtree::build_windows(nodes, shape, depth[e], &wt);
+        st = upload_encoding(wt, &t->enc[e]);
         if (st != DT_OK) {
             free_encoding(&t->enc[0]);
             free_encoding(&t->enc[1]);
             delete t;
             return st;
         }
+    }
+    for (int algo = 0; algo < 3; ++algo) {
+        const Encoding &enc = t->enc[encoding_of(algo)];
         for (int m = 0; m < dtree::kLoadModes; ++m) {
             if (t->row_stride > dtree::kMaxRowStride) {
                 t->plan[algo][m][0].why = t->plan[algo][m][1].why = "n_features > 256";
@@ -403,9 +425,8 @@ dt_status create_impl(const dt_node *nodes, int32_t n_nodes, int32_t n_features,
             if (m == dtree::kLoadExact && n_features != t->row_stride) continue;
             if (m != dtree::kLoadScalar && n_features % 4 != 0) continue;
             for (int o = 0; o < 2; ++o)
-                make_plan(t->caps, algo, t->row_stride, m, t->enc[algo].depth,
-                          t->enc[algo].table_bytes(), o == 0 ? 1 : 4,
-                          opt ? opt->waves_per_cu : 0, &t->plan[algo][m][o]);
+                make_plan(t->caps, algo, t->row_stride, m, enc.depth, enc.table_bytes(),
+                          o == 0 ? 1 : 4, opt ? opt->waves_per_cu : 0, &t->plan[algo][m][o]);
         }
     }
     *out = t;
@@ -652,6 +673,8 @@ dt_status forest_classify_impl(const dt_forest *f, const float *d_x, int64_t n, 
                                void *d_out, dt_output out_kind, dt_algo algo, void *stream) {
     if (!f) return fail(DT_ERR_INVALID_ARG, "forest is NULL");
     if (n < 0) return fail(DT_ERR_INVALID_ARG, "n must be >= 0");
+    if (algo == DT_ALGO_PATH)
+        return fail(DT_ERR_UNSUPPORTED, "forests run the data and speculative decompositions");
     if (algo != DT_ALGO_DATA && algo != DT_ALGO_SPECULATIVE)
         return fail(DT_ERR_INVALID_ARG, "unknown algo");
     if (out_kind != DT_OUT_CLASS_U8 && out_kind != DT_OUT_CLASS_I32)
@@ -800,8 +823,7 @@ dt_status dt_tree_launch_info(const dt_tree *t, const float *d_x, int64_t ld, dt
                               dt_algo algo, dt_launch_info *info) {
     g_last_error.clear();
     if (!t || !info) return fail(DT_ERR_INVALID_ARG, "null argument");
-    if (algo != DT_ALGO_DATA && algo != DT_ALGO_SPECULATIVE)
-        return fail(DT_ERR_INVALID_ARG, "unknown algo");
+    if (!single_tree_algo(algo)) return fail(DT_ERR_INVALID_ARG, "unknown algo");
     if (out_kind != DT_OUT_CLASS_U8 && out_kind != DT_OUT_CLASS_I32 && out_kind != DT_OUT_LEAF_I32)
         return fail(DT_ERR_INVALID_ARG, "unknown out_kind");
     if (ld < t->n_features) return fail(DT_ERR_INVALID_ARG, "ld must be >= n_features");

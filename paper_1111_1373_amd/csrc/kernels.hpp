@@ -36,8 +36,12 @@ struct KArgs {
     int32_t out_kind;        // 0: uint8 output, 1: int32 output
     int32_t out_cap;         // tiles of results each wavefront buffers in the LDS (>= 1)
     int32_t out_vec;         // 1: `out` is 16-byte aligned (flushes use 16-byte stores)
+    int32_t hops;            // path-reduction kernel: further entries read per round
     void *out;
 };
+
+// Path-reduction kernel: per wavefront, 64/S segments of 2S path entries (S lanes each).
+constexpr int kPathIntsPerWave = 128;
 
 // LDS bytes of one wavefront's result buffer: cap tiles of 64 results of out_bytes each.
 __host__ __device__ inline int out_buffer_bytes(int cap, int out_bytes) { return cap * kTileRows * out_bytes; }
@@ -61,7 +65,7 @@ struct FArgs {
     void *out;
 };
 
-enum KernelAlgo { kAlgoData = 0, kAlgoSpec = 1 };
+enum KernelAlgo { kAlgoData = 0, kAlgoSpec = 1, kAlgoPath = 2 };
 
 // How record tiles are read from HBM.
 enum LoadMode {
@@ -76,6 +80,9 @@ enum LoadMode {
 // read from global memory, window depth), or nullptr if no such instance exists.
 // `depth` is ignored by the data kernel.
 const void *kernel_for(int algo, int row_stride, int load_mode, bool tables_in_lds, int depth);
+
+// Path-reduction kernel instance (speculative windows of depth 1..6).
+const void *path_kernel_for(int row_stride, int load_mode, bool tables_in_lds, int depth);
 
 // Forest kernel instance; `vote_words` = 32-bit words of packed 8-bit counters
 // (2, 4 or 16 for up to 8, 16 or 64 classes).

@@ -29,7 +29,7 @@ if not os.path.exists(LIB_PATH):
 _lib = ctypes.CDLL(LIB_PATH)
 
 DT_OK, DT_ERR_INVALID_ARG, DT_ERR_INVALID_TREE, DT_ERR_UNSUPPORTED, DT_ERR_HIP, DT_ERR_NO_MEMORY = range(6)
-ALGOS = {"data": 0, "speculative": 1}
+ALGOS = {"data": 0, "speculative": 1, "path": 2}
 OUT_KINDS = {"class_u8": 0, "class_i32": 1, "leaf_i32": 2}
 
 NODE_DTYPE = np.dtype(
@@ -38,7 +38,7 @@ NODE_DTYPE = np.dtype(
 
 class TreeOptions(ctypes.Structure):
     _fields_ = [("data_window_depth", ctypes.c_int32), ("spec_window_depth", ctypes.c_int32),
-                ("waves_per_cu", ctypes.c_int32)]
+                ("waves_per_cu", ctypes.c_int32), ("path_hops", ctypes.c_int32)]
 
 
 class TreeInfo(ctypes.Structure):
@@ -105,16 +105,18 @@ def _nodes(nodes) -> np.ndarray:
     return arr
 
 
-def _options(data_window_depth: int, spec_window_depth: int, waves_per_cu: int = 0) -> TreeOptions:
-    return TreeOptions(int(data_window_depth), int(spec_window_depth), int(waves_per_cu))
+def _options(data_window_depth: int, spec_window_depth: int, waves_per_cu: int = 0,
+             path_hops: int = 0) -> TreeOptions:
+    return TreeOptions(int(data_window_depth), int(spec_window_depth), int(waves_per_cu),
+                       int(path_hops))
 
 
 def tree_check(nodes, n_features: int, n_classes: int, data_window_depth: int = 0,
-               spec_window_depth: int = 0, waves_per_cu: int = 0) -> dict:
+               spec_window_depth: int = 0, waves_per_cu: int = 0, path_hops: int = 0) -> dict:
     """Validate a tree on the host and describe its encodings (no GPU needed)."""
     nd = _nodes(nodes)
     info = TreeInfo()
-    opt = _options(data_window_depth, spec_window_depth, waves_per_cu)
+    opt = _options(data_window_depth, spec_window_depth, waves_per_cu, path_hops)
     _check(_lib.dt_tree_check(nd.ctypes.data, len(nd), n_features, n_classes,
                               ctypes.byref(opt), ctypes.byref(info)), "dt_tree_check")
     return info.as_dict()
@@ -176,12 +178,12 @@ class Tree:
     """A tree uploaded to the current device (``dt_tree_create``)."""
 
     def __init__(self, nodes, n_features: int, n_classes: int, data_window_depth: int = 0,
-                 spec_window_depth: int = 0, waves_per_cu: int = 0):
+                 spec_window_depth: int = 0, waves_per_cu: int = 0, path_hops: int = 0):
         nd = _nodes(nodes)
         self.n_features = int(n_features)
         self.n_classes = int(n_classes)
         self._h = ctypes.c_void_p()
-        opt = _options(data_window_depth, spec_window_depth, waves_per_cu)
+        opt = _options(data_window_depth, spec_window_depth, waves_per_cu, path_hops)
         _check(_lib.dt_tree_create(nd.ctypes.data, len(nd), n_features, n_classes,
                                    ctypes.byref(opt), ctypes.byref(self._h)), "dt_tree_create")
 

@@ -42,7 +42,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version_and_strings():
-    assert dt.ABI_VERSION == 1
+    assert dt.ABI_VERSION == 2
     for s in range(6):
         assert dt._lib.dt_status_string(s)
     assert dt._lib.dt_status_string(99) == b"unknown status"
@@ -124,6 +124,9 @@ def test_argument_errors():
     assert _status(n, C=0) == dt.DT_ERR_INVALID_ARG
     assert _status(n, spec_window_depth=7) == dt.DT_ERR_INVALID_ARG
     assert _status(n, data_window_depth=17) == dt.DT_ERR_INVALID_ARG
+    assert _status(n, path_hops=9) == dt.DT_ERR_INVALID_ARG
+    assert _status(n, path_hops=-1) == dt.DT_ERR_INVALID_ARG
+    assert _status(n, path_hops=8) == dt.DT_OK
     assert dt._lib.dt_tree_check(None, 3, 2, 4, None, None) == dt.DT_ERR_INVALID_ARG
     assert dt._lib.dt_tree_check(n.ctypes.data, 0, 2, 4, None, None) == dt.DT_ERR_INVALID_ARG
     assert b"n_nodes" in dt._lib.dt_last_error()
@@ -199,6 +202,45 @@ def walk_tables_mask(tab, x, exits_key="exit_class"):
     return -code - 1
 
 
+def walk_tables_path(tab, x, hops, exits_key="exit_class"):
+    """Path-array form (Procedure 5): per record and window, entry j of a 2^(D+1) array
+    names the child slot j's predicate chose, bottom positions point to themselves, and
+    every round replaces each entry by the one `hops` further along until the root's
+    entry is a bottom position.  Returns the classes and the most rounds any window took."""
+    D = tab["depth"]
+    S = 1 << D
+    n = x.shape[0]
+    rows = np.arange(n)
+    w = np.zeros(n, dtype=np.int64)
+    code = np.zeros(n, dtype=np.int64)
+    done = np.zeros(n, dtype=bool)
+    most = 0
+    j = np.arange(1, S)
+    for _ in range(tab["levels"]):
+        f = tab["feature"][w]
+        t = tab["threshold"][w]
+        bits = ~(x[rows[:, None], f] < t)
+        path = np.empty((n, 2 * S), dtype=np.int64)
+        path[:, 0] = 0
+        path[:, S:] = np.arange(S, 2 * S)
+        path[:, 1:S] = 2 * j + bits[:, 1:S]
+        rounds = 0
+        while not (path[:, 1] >= S).all():
+            assert rounds < D
+            v = path[:, 1:S]
+            for _ in range(hops):
+                v = np.take_along_axis(path, v, axis=1)
+            path[:, 1:S] = v                       # every entry updated from the old array
+            rounds += 1
+        most = max(most, rounds)
+        c = tab[exits_key][w, path[:, 1] - S].astype(np.int64)
+        code = np.where(done, code, c)
+        done |= c < 0
+        w = np.where(done, w, np.maximum(c, 0))
+    assert done.all()
+    return -code - 1, most
+
+
 def _tree_cases():
     r = np.random.Generator(np.random.PCG64(77))
     cases = []
@@ -233,6 +275,15 @@ def test_window_tables_reproduce_oracle(case, depth):
     if depth <= 6:
         np.testing.assert_array_equal(walk_tables_mask(tab, x), want_cls)
         np.testing.assert_array_equal(walk_tables_mask(tab, x, "exit_leaf"), want_leaf)
+        for hops in (1, 2, 3):
+            got, most = walk_tables_path(tab, x, hops)
+            np.testing.assert_array_equal(got, want_cls)
+            # reach (hops + 1)^r after r rounds: the D levels of a window need at most
+            # ceil(log_(hops+1) D) rounds
+            bound = 0
+            while (hops + 1) ** bound < depth:
+                bound += 1
+            assert most <= bound
 
 
 @pytest.mark.parametrize("d,D", [(4, 4), (8, 4), (12, 6), (12, 4), (12, 12), (10, 3), (5, 2)])

@@ -105,3 +105,6 @@ def test_forest_argument_errors(dt):
     out = torch.empty(10, dtype=torch.uint8, device="cuda")
     assert dt._lib.dt_forest_classify(f._h, x.data_ptr(), 10, 31, out.data_ptr(), 0, 0, None) == dt.DT_ERR_INVALID_ARG
     assert dt._lib.dt_forest_classify(f._h, x.data_ptr(), 0, 32, out.data_ptr(), 0, 0, None) == dt.DT_OK
+    # the path-array kernel is a single-tree decomposition
+    assert dt._lib.dt_forest_classify(f._h, x.data_ptr(), 10, 32, out.data_ptr(), 0, 2, None) == dt.DT_ERR_UNSUPPORTED
+    assert dt._lib.dt_forest_classify(f._h, x.data_ptr(), 10, 32, out.data_ptr(), 0, 3, None) == dt.DT_ERR_INVALID_ARG
