@@ -1,6 +1,6 @@
 """Counter calibration run: a streaming copy of exactly known size.
 
-    python -m paper_1111_1373_amd.calibrate [--mib 1024] [--reps 5]
+    python paper_1111_1373_amd/calibrate.py [--mib 1024] [--reps 5]
 
 Launches the library's copy kernel (dt_probe_copy) `reps` times on a buffer of `mib`
 MiB and prints the bytes each launch reads and writes, and the bandwidth it reaches.
@@ -9,10 +9,15 @@ by the known byte counts give the scale factors applied to the tree kernels' cou
 """
 import argparse
 import json
+import os
+import sys
 
-import torch
+if __package__ in (None, ""):   # run as a script: make the package importable
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
 
-from paper_1111_1373_amd import dtree as dt
+import torch  # noqa: E402
+
+from paper_1111_1373_amd import dtree as dt  # noqa: E402
 
 
 def main():
