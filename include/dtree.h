@@ -238,6 +238,78 @@ void dt_forest_destroy(dt_forest *forest);
 dt_status dt_forest_classify(const dt_forest *forest, const float *d_x, int64_t n, int64_t ld,
                              void *d_out, dt_output out_kind, dt_algo algo, void *stream);
 
+/* ---- host-resident records: the outer-time path -------------------------------------
+ *
+ * Section 4.2 times each GPU function twice: the "outer" time of the whole call (device
+ * allocation, host-to-device copy of the records, kernel, copy of the labels back, free)
+ * and the "inner" time of the kernel alone; Section 4.3 finds the serial copies dominate
+ * and names pinned host buffers and copies overlapped with computation as the remedy.
+ * A dt_pipeline does that for records that live in host memory: it owns n_slots device
+ * chunk buffers (and pinned bounce buffers), and for each chunk of chunk_rows records it
+ * copies the rows in, classifies them and copies the labels out on the slot's own
+ * stream, so the copies of one chunk overlap the kernel and the copies of the others.
+ * With `serial` set it instead does what Section 4.2 describes: allocate device buffers
+ * for all n records, copy in, classify, copy out and free, one step after the other.
+ */
+typedef struct dt_pipeline dt_pipeline;
+
+typedef struct {
+    int64_t chunk_rows;   /* records per chunk (0: about 32 MiB of features; rounded up
+                             to a multiple of 64) */
+    int32_t n_slots;      /* chunks in flight, 1..8 (0 = 3) */
+    int32_t serial;       /* 1: per-call allocation and serial copies, as Section 4.2;
+                             chunk_rows, n_slots and host_threads are then unused */
+    int32_t host_threads; /* host threads that copy pageable records into the pinned
+                             buffers, 1..16 (0 = 4) */
+} dt_pipeline_options;
+
+/* Timing of a call, host wall clock and HIP events (microseconds).  Chunks overlap, so
+ * the per-step sums can exceed outer_us. */
+typedef struct {
+    double outer_us;      /* wall clock of the whole call, copies included              */
+    double kernel_us;     /* sum over chunks of the classify kernel's duration          */
+    double h2d_us;        /* sum over chunks of the record copy's duration              */
+    double d2h_us;        /* sum over chunks of the label copy's duration               */
+    int64_t chunks;
+    int32_t input_pinned; /* 1: the records were copied straight from the caller's
+                             buffer (page-locked); 0: through pinned bounce buffers     */
+    int32_t output_pinned;
+} dt_pipeline_stats;
+
+/*
+ * Pipeline for records of n_features floats, on the current device.  Allocates its device
+ * and pinned host buffers and creates its streams (default priority) here, never in a
+ * call (unless `serial`).  opt may be NULL.
+ * Errors: DT_ERR_INVALID_ARG (null out, n_features not 1..256, option out of range),
+ * DT_ERR_NO_MEMORY, DT_ERR_HIP.
+ */
+dt_status dt_pipeline_create(int32_t n_features, const dt_pipeline_options *opt,
+                             dt_pipeline **out);
+
+/* Free a pipeline (waits for its streams first).  NULL is a no-op. */
+void dt_pipeline_destroy(dt_pipeline *pipeline);
+
+/*
+ * Labels of n host-resident records (h_x: n rows of the tree's n_features floats, row
+ * stride ld >= n_features floats) written to the host buffer h_out (n uint8 or int32
+ * values).  Synchronous: returns when h_out is complete; the buffers are only read and
+ * written during the call.  Page-locked buffers (allocated with hipHostMalloc, or
+ * torch's pin_memory) are copied by DMA directly; others are staged through the
+ * pipeline's pinned buffers by the host.  A pipeline serves one call at a time.
+ * stats may be NULL.
+ * Errors: those of dt_classify; DT_ERR_INVALID_ARG also for a null pipeline or a tree of
+ * another n_features or device than the pipeline's.  On an error no copy or kernel of
+ * the call is left running.
+ */
+dt_status dt_classify_host(const dt_tree *tree, dt_pipeline *pipeline, const float *h_x,
+                           int64_t n, int64_t ld, void *h_out, dt_output out_kind,
+                           dt_algo algo, dt_pipeline_stats *stats);
+
+/* As dt_classify_host for a forest's majority vote (dt_forest_classify). */
+dt_status dt_forest_classify_host(const dt_forest *forest, dt_pipeline *pipeline,
+                                  const float *h_x, int64_t n, int64_t ld, void *h_out,
+                                  dt_output out_kind, dt_algo algo, dt_pipeline_stats *stats);
+
 #ifdef __cplusplus
 }
 #endif

@@ -13,6 +13,7 @@
 #include "dtree.h"
 #include "encode.hpp"
 #include "kernels.hpp"
+#include "library.hpp"
 
 namespace {
 
@@ -716,6 +717,18 @@ dt_status forest_classify_impl(const dt_forest *f, const float *d_x, int64_t n, 
 }
 
 }  // namespace
+
+namespace dtree {
+
+dt_status set_error(dt_status s, const std::string &msg) { return fail(s, msg); }
+dt_status set_hip_error(hipError_t e, const char *what) { return hip_fail(e, what); }
+void clear_error() { g_last_error.clear(); }
+int device_of(const dt_tree *t) { return t->caps.device; }
+int device_of(const dt_forest *f) { return f->caps.device; }
+int32_t features_of(const dt_tree *t) { return t->n_features; }
+int32_t features_of(const dt_forest *f) { return f->n_features; }
+
+}  // namespace dtree
 
 extern "C" {
 

@@ -52,6 +52,21 @@ class TreeInfo(ctypes.Structure):
         return {f: getattr(self, f) for f, _ in self._fields_}
 
 
+class PipelineOptions(ctypes.Structure):
+    _fields_ = [("chunk_rows", ctypes.c_int64), ("n_slots", ctypes.c_int32),
+                ("serial", ctypes.c_int32), ("host_threads", ctypes.c_int32)]
+
+
+class PipelineStats(ctypes.Structure):
+    _fields_ = [("outer_us", ctypes.c_double), ("kernel_us", ctypes.c_double),
+                ("h2d_us", ctypes.c_double), ("d2h_us", ctypes.c_double),
+                ("chunks", ctypes.c_int64), ("input_pinned", ctypes.c_int32),
+                ("output_pinned", ctypes.c_int32)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
 class LaunchInfo(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "waves_per_workgroup", "workgroups_per_cu", "lds_bytes", "result_buffer_tiles",
@@ -77,6 +92,10 @@ _PROTOS = {
     "dt_forest_destroy": (None, [_p]),
     "dt_forest_classify": (ctypes.c_int, [_p, _p, _i64, _i64, _p, ctypes.c_int, ctypes.c_int, _p]),
     "dt_probe_copy": (ctypes.c_int, [_p, _p, _i64, _p]),
+    "dt_pipeline_create": (ctypes.c_int, [_i32, _p, _p]),
+    "dt_pipeline_destroy": (None, [_p]),
+    "dt_classify_host": (ctypes.c_int, [_p, _p, _p, _i64, _i64, _p, ctypes.c_int, ctypes.c_int, _p]),
+    "dt_forest_classify_host": (ctypes.c_int, [_p, _p, _p, _i64, _i64, _p, ctypes.c_int, ctypes.c_int, _p]),
 }
 for _name, (_res, _args) in _PROTOS.items():
     _f = getattr(_lib, _name)
@@ -265,3 +284,81 @@ def probe_copy(src, dst, stream=None):
         raise ValueError("size mismatch")
     _check(_lib.dt_probe_copy(src.data_ptr(), dst.data_ptr(), nbytes, _stream_handle(stream)),
            "dt_probe_copy")
+
+
+def _host_features_arg(x, n_features: int):
+    """(pointer, rows, row stride in floats) of a host float32 matrix (numpy or CPU tensor)."""
+    import torch
+    if isinstance(x, torch.Tensor):
+        if x.device.type != "cpu":
+            raise TypeError("host features must be a CPU tensor or a numpy array")
+        if x.dtype != torch.float32 or x.dim() != 2:
+            raise TypeError("features must be a 2-D float32 array")
+        rows, cols, st0, st1, ptr = x.shape[0], x.shape[1], x.stride(0), x.stride(1), x.data_ptr()
+    else:
+        if not isinstance(x, np.ndarray) or x.dtype != np.float32 or x.ndim != 2:
+            raise TypeError("features must be a 2-D float32 array")
+        rows, cols, ptr = x.shape[0], x.shape[1], x.ctypes.data
+        st0, st1 = x.strides[0] // 4, x.strides[1] // 4
+        if x.strides[0] % 4 or x.strides[1] % 4:
+            raise ValueError("feature strides must be whole floats")
+    if cols < n_features:
+        raise ValueError("features has %d columns, tree needs %d" % (cols, n_features))
+    if st1 != 1 and cols > 1:
+        raise ValueError("feature rows must be contiguous")
+    ld = st0 if rows > 1 else max(cols, n_features)
+    if ld < n_features:
+        raise ValueError("row stride smaller than n_features")
+    return ptr, rows, ld
+
+
+class Pipeline:
+    """Classification of host-resident records (``dt_pipeline_create`` and
+    ``dt_classify_host``): chunked copies overlapped with the kernels, or with
+    ``serial=True`` per-call allocation and serial copies."""
+
+    def __init__(self, n_features: int, chunk_rows: int = 0, n_slots: int = 0,
+                 serial: bool = False, host_threads: int = 0):
+        self.n_features = int(n_features)
+        self._h = ctypes.c_void_p()
+        opt = PipelineOptions(int(chunk_rows), int(n_slots), 1 if serial else 0, int(host_threads))
+        _check(_lib.dt_pipeline_create(self.n_features, ctypes.byref(opt), ctypes.byref(self._h)),
+               "dt_pipeline_create")
+        self.last_stats = None
+
+    def classify(self, model, x, algo: str = "data", out_kind: str = "class_u8", out=None):
+        """Labels of the rows of the host matrix ``x`` for a :class:`Tree` or :class:`Forest`,
+        in ``out`` (host, allocated if None: numpy for numpy input, else a CPU tensor).
+        Timing of the call is left in ``self.last_stats``."""
+        import torch
+        ptr, n, ld = _host_features_arg(x, self.n_features)
+        np_dtype = np.uint8 if out_kind == "class_u8" else np.int32
+        if out is None:
+            out = (np.empty(n, dtype=np_dtype) if isinstance(x, np.ndarray)
+                   else torch.empty(n, dtype=torch.uint8 if out_kind == "class_u8" else torch.int32))
+        if isinstance(out, np.ndarray):
+            if out.dtype != np_dtype or out.size != n or not out.flags.c_contiguous:
+                raise ValueError("out must be a contiguous %s array of %d elements" % (np_dtype, n))
+            optr = out.ctypes.data
+        else:
+            want = torch.uint8 if out_kind == "class_u8" else torch.int32
+            if out.dtype != want or out.numel() != n or not out.is_contiguous() or out.device.type != "cpu":
+                raise ValueError("out must be a contiguous CPU %s tensor of %d elements" % (want, n))
+            optr = out.data_ptr()
+        st = PipelineStats()
+        fn = _lib.dt_forest_classify_host if isinstance(model, Forest) else _lib.dt_classify_host
+        _check(fn(model._h, self._h, ptr if n else None, n, ld, optr if n else None,
+                  OUT_KINDS[out_kind], ALGOS[algo], ctypes.byref(st)), fn.__name__)
+        self.last_stats = st.as_dict()
+        return out
+
+    def close(self):
+        if self._h:
+            _lib.dt_pipeline_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -337,3 +337,19 @@ def test_forest_argument_errors():
     bad[4] = (0, 0.0, -1, 9)                                                # class >= C
     assert _forest_status(bad, [0, 3, 6]) == dt.DT_ERR_INVALID_TREE
     assert b"tree 1" in dt._lib.dt_last_error()
+
+
+def test_pipeline_argument_errors_on_host():
+    """Pipeline options are checked before any device call."""
+    h = ctypes.c_void_p()
+    bad = [(0, dt.PipelineOptions(0, 0, 0, 0)), (257, dt.PipelineOptions(0, 0, 0, 0)),
+           (8, dt.PipelineOptions(-1, 0, 0, 0)), (8, dt.PipelineOptions(0, 9, 0, 0)),
+           (8, dt.PipelineOptions(0, -1, 0, 0)), (8, dt.PipelineOptions(0, 0, 2, 0)),
+           (8, dt.PipelineOptions(0, 0, 0, 17)), (8, dt.PipelineOptions(0, 0, 0, -1))]
+    for F, opt in bad:
+        assert dt._lib.dt_pipeline_create(F, ctypes.byref(opt), ctypes.byref(h)) == dt.DT_ERR_INVALID_ARG
+        assert not h.value
+    assert dt._lib.dt_pipeline_create(8, None, None) == dt.DT_ERR_INVALID_ARG
+    assert dt._lib.dt_classify_host(None, None, None, 0, 8, None, 0, 0, None) == dt.DT_ERR_INVALID_ARG
+    assert dt._lib.dt_forest_classify_host(None, None, None, 0, 8, None, 0, 0, None) == dt.DT_ERR_INVALID_ARG
+    assert dt._lib.dt_pipeline_destroy(None) is None

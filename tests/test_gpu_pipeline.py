@@ -1,0 +1,156 @@
+"""GPU parity of the host-resident path (dt_classify_host / dt_forest_classify_host).
+
+Records start in host memory (pageable numpy arrays or page-locked torch tensors), go
+through the pipeline's chunked copies and the same kernels, and the labels that come back
+must equal the oracle's element by element.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_1111_1373_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def dt():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_1111_1373_amd import dtree   # raises ImportError if the library is missing
+    return dtree
+
+
+@pytest.fixture(scope="module")
+def c3():
+    w = W.config(3, n_samples=200_003)       # not a multiple of any chunk size below
+    x = w.features()
+    return w, x, oracle.tree_classes(w.nodes, x, w.n_features), oracle.tree_leaves(
+        w.nodes, x, w.n_features)
+
+
+@pytest.mark.parametrize("pinned", [False, True])
+@pytest.mark.parametrize("chunk_rows,n_slots", [(0, 0), (1000, 1), (4096, 2), (20_000, 3), (7000, 8)])
+def test_tree_chunks_and_slots(dt, c3, pinned, chunk_rows, n_slots):
+    w, x, want, _ = c3
+    t = dt.Tree(w.nodes, w.n_features, w.n_classes)
+    p = dt.Pipeline(w.n_features, chunk_rows=chunk_rows, n_slots=n_slots)
+    xin = torch.from_numpy(x).pin_memory() if pinned else x
+    got = p.classify(t, xin, algo="data")
+    got = got.numpy() if isinstance(got, torch.Tensor) else got
+    np.testing.assert_array_equal(got.astype(np.int32), want)
+    st = p.last_stats
+    print("chunks", chunk_rows, n_slots, pinned, st, flush=True)
+    assert st["input_pinned"] == int(pinned)
+    rows = chunk_rows if chunk_rows else max(1, (32 << 20) // (4 * w.n_features))
+    rows = (rows + 63) // 64 * 64
+    assert st["chunks"] == -(-x.shape[0] // rows)
+    assert st["outer_us"] > 0 and st["kernel_us"] > 0 and st["h2d_us"] > 0
+
+
+@pytest.mark.parametrize("algo", ["data", "speculative", "path"])
+@pytest.mark.parametrize("out_kind", ["class_u8", "class_i32", "leaf_i32"])
+def test_tree_algos_and_outputs(dt, c3, algo, out_kind):
+    w, x, want, want_leaf = c3
+    t = dt.Tree(w.nodes, w.n_features, w.n_classes)
+    p = dt.Pipeline(w.n_features, chunk_rows=16_384)
+    got = p.classify(t, x, algo=algo, out_kind=out_kind)
+    np.testing.assert_array_equal(got.astype(np.int32), want_leaf if out_kind == "leaf_i32" else want)
+
+
+def test_pinned_output_and_strided_input(dt, c3):
+    w, x, want, _ = c3
+    F = w.n_features
+    wide = np.zeros((x.shape[0], F + 5), dtype=np.float32)
+    wide[:, :F] = x
+    wide[:, F:] = np.nan          # columns past n_features must never be read
+    t = dt.Tree(w.nodes, F, w.n_classes)
+    p = dt.Pipeline(F, chunk_rows=5000)
+    for xin in (wide, torch.from_numpy(wide).pin_memory()):
+        out = torch.empty(x.shape[0], dtype=torch.uint8).pin_memory()
+        got = p.classify(t, xin, out=out)
+        assert got is out and p.last_stats["output_pinned"] == 1
+        np.testing.assert_array_equal(out.numpy().astype(np.int32), want)
+        got = p.classify(t, xin[1:-1])           # offset start, ragged length
+        got = got.numpy() if isinstance(got, torch.Tensor) else got
+        np.testing.assert_array_equal(got.astype(np.int32), want[1:-1])
+
+
+@pytest.mark.parametrize("pinned", [False, True])
+def test_serial_scheme(dt, c3, pinned):
+    """Per-call allocation and serial copies (the scheme timed in Section 4.2)."""
+    w, x, want, _ = c3
+    t = dt.Tree(w.nodes, w.n_features, w.n_classes)
+    p = dt.Pipeline(w.n_features, serial=True)
+    xin = torch.from_numpy(x).pin_memory() if pinned else x
+    for algo in ("data", "speculative"):
+        got = p.classify(t, xin, algo=algo)
+        got = got.numpy() if isinstance(got, torch.Tensor) else got
+        np.testing.assert_array_equal(got.astype(np.int32), want)
+        assert p.last_stats["chunks"] == 1
+
+
+def test_forest(dt):
+    w = W.config(5, n_samples=150_001)
+    x = w.features()
+    want = oracle.forest_classes(w.nodes, w.tree_offsets, x, w.n_features, w.n_classes)
+    f = dt.Forest(w.nodes, w.tree_offsets, w.n_features, w.n_classes)
+    for serial in (False, True):
+        p = dt.Pipeline(w.n_features, chunk_rows=0 if serial else 10_000, serial=serial)
+        for algo in ("data", "speculative"):
+            got = p.classify(f, x, algo=algo, out_kind="class_i32")
+            np.testing.assert_array_equal(got, want)
+    with pytest.raises(dt.DTreeError) as e:
+        p.classify(f, x, algo="path")
+    assert e.value.status == dt.DT_ERR_UNSUPPORTED
+
+
+def test_empty_and_single_row(dt):
+    w = W.config(2, n_samples=1)
+    x = w.features()
+    t = dt.Tree(w.nodes, w.n_features, w.n_classes)
+    p = dt.Pipeline(w.n_features)
+    assert p.classify(t, x[:0]).size == 0
+    assert p.last_stats["chunks"] == 0
+    got = p.classify(t, x)
+    np.testing.assert_array_equal(got.astype(np.int32), oracle.tree_classes(w.nodes, x, w.n_features))
+
+
+def test_errors(dt, c3):
+    w, x, _, _ = c3
+    t = dt.Tree(w.nodes, w.n_features, w.n_classes)
+    p = dt.Pipeline(w.n_features + 1)
+    with pytest.raises(dt.DTreeError) as e:
+        p.classify(t, np.zeros((10, w.n_features + 1), dtype=np.float32))
+    assert e.value.status == dt.DT_ERR_INVALID_ARG
+    p = dt.Pipeline(w.n_features)
+    out = np.zeros(10, dtype=np.uint8)
+    bad_kind = dt._lib.dt_classify_host(t._h, p._h, x.ctypes.data, 10, w.n_features,
+                                        out.ctypes.data, 7, 0, None)
+    assert bad_kind == dt.DT_ERR_INVALID_ARG
+    bad_ld = dt._lib.dt_classify_host(t._h, p._h, x.ctypes.data, 10, w.n_features - 1,
+                                      out.ctypes.data, 0, 0, None)
+    assert bad_ld == dt.DT_ERR_INVALID_ARG
+    assert (out == 0).all()                       # nothing written on an argument error
+    # the pipeline still works after errors
+    got = p.classify(t, x[:1000])
+    np.testing.assert_array_equal(got.astype(np.int32),
+                                  oracle.tree_classes(w.nodes, x[:1000], w.n_features))
+
+
+@pytest.mark.parametrize("host_threads", [1, 3, 16])
+def test_host_packing_threads(dt, c3, host_threads):
+    """Pageable records packed into the pinned buffers by 1..16 host threads (chunks of
+    several MiB, so every thread gets a slice), with a row stride wider than F."""
+    w, x, want, _ = c3
+    F = w.n_features
+    wide = np.full((x.shape[0], F + 3), np.inf, dtype=np.float32)
+    wide[:, :F] = x
+    t = dt.Tree(w.nodes, F, w.n_classes)
+    for xin, ref in ((x, want), (wide, want), (x[7:], want[7:])):
+        p = dt.Pipeline(F, chunk_rows=60_000, host_threads=host_threads)
+        got = p.classify(t, xin, algo="speculative")
+        np.testing.assert_array_equal(got.astype(np.int32), ref)
+        assert p.last_stats["input_pinned"] == 0
