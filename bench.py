@@ -121,6 +121,8 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU time spent timing the oracle")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-narrow", dest="narrow", action="store_false",
+                    help="skip the fp16 / bf16 / uint8 record runs")
     ap.add_argument("--outer-reps", type=int, default=3,
                     help="calls per host-resident scheme timed for the outer time (0: skip)")
     args = ap.parse_args()
@@ -192,23 +194,27 @@ def main() -> int:
     feature_bytes = n * F * 4
     algo_bytes = feature_bytes + n * 1          # fp32 features read + uint8 labels written
     results = {}
-    for algo in algos:
+    def timed(model, xd, algo, steps, warmup):
+        """(wall seconds of `steps` launches, per-launch kernel seconds, labels)."""
         out = torch.empty(n, dtype=torch.uint8, device="cuda")
-        for _ in range(args.warmup):
-            tree.classify(x, algo=algo, out=out, stream=stream)
+        for _ in range(warmup):
+            model.classify(xd, algo=algo, out=out, stream=stream)
         torch.cuda.synchronize()
-        ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-        ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+        ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+        ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        for i in range(args.steps):
+        for i in range(steps):
             ev0[i].record(stream)
-            tree.classify(x, algo=algo, out=out, stream=stream)
+            model.classify(xd, algo=algo, out=out, stream=stream)
             ev1[i].record(stream)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
         ks = np.array([a.elapsed_time(b) for a, b in zip(ev0, ev1)]) * 1e-3   # seconds
-        got = out.cpu().numpy().astype(np.int32)
+        return wall, ks, out.cpu().numpy().astype(np.int32)
+
+    for algo in algos:
+        wall, ks, got = timed(tree, x, algo, args.steps, args.warmup)
         mism = int((got != want).sum())
         kavg = float(ks.mean())
         results[algo] = {
@@ -232,6 +238,42 @@ def main() -> int:
         log(algo, json.dumps(results[algo]))
         if mism:
             log("PARITY FAILURE:", algo, mism, "mismatches")
+
+    narrow = None
+    if not w.is_forest and args.narrow:
+        narrow = {}
+        for xt in W.NARROW_TYPES:
+            xn = W.narrow_records(x_np, xt, w.feature_dist)
+            nodes_n = W.narrow_tree(w.nodes, xt, w.feature_dist)
+            xw = xn.astype(np.float32) if xt != "bf16" else \
+                (xn.astype(np.uint32) << np.uint32(16)).view(np.float32)
+            want_n = oracle.tree_classes(nodes_n, xw, F)
+            del xw
+            xd = torch.from_numpy(xn)
+            if xt == "bf16":
+                xd = xd.view(torch.int16).view(torch.bfloat16)
+            xd = xd.cuda()
+            tree_n = dt.Tree(nodes_n, w.n_features, w.n_classes,
+                             data_window_depth=args.data_window_depth,
+                             spec_window_depth=args.spec_window_depth,
+                             waves_per_cu=args.waves_per_cu)
+            esize = xn.dtype.itemsize
+            narrow[xt] = {}
+            for algo in ("data", "speculative"):
+                wall, ks, got = timed(tree_n, xd, algo, args.steps, args.warmup)
+                kavg = float(ks.mean())
+                bytes_n = n * (F * esize + 1)
+                narrow[xt][algo] = {
+                    "kernel_us": kavg * 1e6, "kernel_samples_per_s": n / kavg,
+                    "samples_per_s": n / (wall / args.steps),
+                    "algorithmic_bytes_per_launch": bytes_n,
+                    "hbm_gbps": bytes_n / kavg / 1e9,
+                    "frac_of_peak": bytes_n / kavg / 1e9 / PEAK_HBM_GBPS,
+                    "mismatches_vs_oracle": int((got != want_n).sum()),
+                    "launch": tree_n.launch_info(xd, algo=algo, out_kind="class_u8"),
+                }
+                log("narrow", xt, algo, json.dumps(narrow[xt][algo]))
+            del xd, tree_n
 
     outer = None
     if args.outer_reps > 0:
@@ -267,7 +309,9 @@ def main() -> int:
         "parity": "bit-exact vs oracle on all %d records" % n
                   if all(v["mismatches_vs_oracle"] == 0 for v in results.values()) and
                   (outer is None or
-                   all(v["mismatches_vs_oracle"] == 0 for v in outer["schemes"].values()))
+                   all(v["mismatches_vs_oracle"] == 0 for v in outer["schemes"].values())) and
+                  (narrow is None or
+                   all(r["mismatches_vs_oracle"] == 0 for v in narrow.values() for r in v.values()))
                   else "MISMATCH",
         "decompositions": results,
         "speculative_over_data_kernel_time": (
@@ -276,6 +320,7 @@ def main() -> int:
         "path_over_speculative_kernel_time": (
             results["path"]["kernel_us"]["avg"] / results["speculative"]["kernel_us"]["avg"]
             if "path" in results and "speculative" in results else None),
+        "narrow_records": narrow,
         "outer_time": outer,
         "paper_context": PAPER_CONTEXT,
         "source_hash": kernel_source_hash("forest" if w.is_forest else best),

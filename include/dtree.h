@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define DT_ABI_VERSION 2
+#define DT_ABI_VERSION 3
 
 typedef enum {
     DT_OK = 0,
@@ -70,6 +70,20 @@ typedef enum {
     DT_OUT_LEAF_I32 = 2       /* int32_t index (in the node array) of the leaf reached;
                                  single trees only                                          */
 } dt_output;
+
+/*
+ * Element type of the records (dt_classify_typed).  Section 2.1 treats continuous
+ * attributes as real values carried in floating point and notes that ordered discrete
+ * values behave the same; narrower record types cut the bytes read per record.  Every
+ * element is widened exactly to fp32 and compared with the fp32 threshold, so the result
+ * is the fp32 result for the widened records.
+ */
+typedef enum {
+    DT_F32 = 0,               /* IEEE binary32                                              */
+    DT_F16 = 1,               /* IEEE binary16 (bits in a uint16)                           */
+    DT_BF16 = 2,              /* bfloat16: the upper 16 bits of a binary32                  */
+    DT_U8 = 3                 /* uint8: ordered discrete values 0..255                      */
+} dt_dtype;
 
 /* One node of the breadth-first array (Procedure 1).  16 bytes, no padding. */
 typedef struct {
@@ -188,11 +202,13 @@ typedef struct {
                                       of rows exactly one LDS row stride wide            */
 } dt_launch_info;
 
-/* Fill *info with the launch shape of dt_classify(tree, d_x, n, ld, ..., out_kind, algo)
- * for any n > 0.  Only the alignment of d_x is read.  Errors: DT_ERR_INVALID_ARG (null,
- * unknown enum, ld < n_features), or the error classify would return for this shape. */
-dt_status dt_tree_launch_info(const dt_tree *tree, const float *d_x, int64_t ld,
-                              dt_output out_kind, dt_algo algo, dt_launch_info *info);
+/* Fill *info with the launch shape of dt_classify_typed(tree, d_x, x_type, n, ld, ...,
+ * out_kind, algo) for any n > 0.  Only the alignment of d_x is read.  Errors:
+ * DT_ERR_INVALID_ARG (null, unknown enum, ld < n_features), or the error classify would
+ * return for this shape. */
+dt_status dt_tree_launch_info(const dt_tree *tree, const void *d_x, dt_dtype x_type,
+                              int64_t ld, dt_output out_kind, dt_algo algo,
+                              dt_launch_info *info);
 
 /*
  * Classify n records.  Asynchronous on `stream` (a hipStream_t; NULL = the null stream).
@@ -214,6 +230,18 @@ dt_status dt_tree_launch_info(const dt_tree *tree, const float *d_x, int64_t ld,
  */
 dt_status dt_classify(const dt_tree *tree, const float *d_x, int64_t n, int64_t ld,
                       void *d_out, dt_output out_kind, dt_algo algo, void *stream);
+
+/*
+ * dt_classify for records of element type x_type (dt_dtype): d_x must be aligned to the
+ * element size and ld counts elements.  Rows that are contiguous, 16-byte aligned and a
+ * multiple of 16 bytes long take the vectorised load path.  Each element is widened
+ * exactly to fp32 before its comparison, so the labels equal those of dt_classify on the
+ * widened records.  DT_ALGO_PATH reads DT_F32 records only (DT_ERR_UNSUPPORTED otherwise).
+ * Errors: as dt_classify, and DT_ERR_INVALID_ARG for an unknown x_type or a misaligned d_x.
+ */
+dt_status dt_classify_typed(const dt_tree *tree, const void *d_x, dt_dtype x_type, int64_t n,
+                            int64_t ld, void *d_out, dt_output out_kind, dt_algo algo,
+                            void *stream);
 
 /*
  * Forest of n_trees trees: tree k occupies nodes[tree_offsets[k] .. tree_offsets[k+1])

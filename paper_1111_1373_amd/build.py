@@ -18,7 +18,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libdtree.so")
 OBJDIR = os.path.join(HERE, "_build")
-SOURCES = ["dtree.hip", "kernels.hip", "forest.hip", "probe.hip", "path.hip", "encode.cpp", "pipeline.cpp"]
+SOURCES = ["dtree.hip", "kernels.hip", "kernels_f16.hip", "kernels_bf16.hip", "kernels_u8.hip",
+           "forest.hip", "probe.hip", "path.hip", "encode.cpp", "pipeline.cpp"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -1,10 +1,13 @@
 // Device building blocks shared by the single-tree and forest kernels (gfx950).
 //
 // Record tiles: every wavefront owns a private tile of 64 records (one per lane) in the
-// LDS.  Row r (record) starts at r*RS floats; column c is stored at position c ^ swz(r).
-// The XOR spreads the 64 rows over all 64 banks for a fixed column, so the top levels of
-// a tree (where every lane reads the same feature) are conflict-free, and the 16-byte
-// staging stores land on distinct banks.
+// LDS, in the records' own element type (fp32, fp16, bf16 or uint8).  Row r (record)
+// starts at element r*RS; the 4-byte word w of a row is stored at word w ^ swz(r), bytes
+// within a word unchanged.  The XOR spreads the 64 rows over all 64 banks for a fixed
+// column, so the top levels of a tree (where every lane reads the same feature) are
+// conflict-free, and the staging stores land on distinct banks.  Staging moves whole
+// words and does not depend on the element type; a tree step widens the element it reads
+// to fp32 (exactly) and compares it with the fp32 threshold.
 //
 // Window tables (built on the host, see encode.hpp): for window w, slot p in [1, 2^D)
 // holds the (threshold, feature) of heap node p (children 2p, 2p+1; slot 0 is padding);
@@ -33,14 +36,48 @@ struct alignas(16) Slot2 {
     Slot l, r;
 };
 
-template <int RS>
+// Word swizzle of row r for rows of RSW 4-byte words.
+template <int RSW>
 __device__ __forceinline__ int swz(int r) {
-    if constexpr (RS >= 64) {
-        return r;                                  // r < 64 <= RS
+    if constexpr (RSW >= 64) {
+        return r;                                  // r < 64 <= RSW
     } else {
-        constexpr int sh = __builtin_ctz(64 / RS);
-        return (r >> sh) & (RS - 1);
+        constexpr int sh = __builtin_ctz(64 / RSW);
+        return (r >> sh) & (RSW - 1);
     }
+}
+
+// Record element types.  widen() is exact for every value (NaN stays NaN, fp16 and bf16
+// subnormals become the same fp32 value), so a decision on a widened element is the
+// decision on the value the element stores.
+template <int XT> struct Elem;
+template <> struct Elem<kXF32> {
+    using T = float;
+    static __device__ __forceinline__ float widen(float v) { return v; }
+};
+template <> struct Elem<kXF16> {
+    using T = uint16_t;   // IEEE binary16 bits
+    static __device__ __forceinline__ float widen(uint16_t b) {
+        return float(__builtin_bit_cast(_Float16, b));
+    }
+};
+template <> struct Elem<kXBF16> {
+    using T = uint16_t;   // bfloat16 bits: the high half of an fp32
+    static __device__ __forceinline__ float widen(uint16_t b) {
+        return __uint_as_float(uint32_t(b) << 16);
+    }
+};
+template <> struct Elem<kXU8> {
+    using T = uint8_t;
+    static __device__ __forceinline__ float widen(uint8_t b) { return float(b); }
+};
+
+// Element-level position swizzle for rows of RS elements of type XT: the word swizzle,
+// scaled to elements (the position of an element within its word is unchanged).
+template <int XT, int RS>
+__device__ __forceinline__ int swz_el(int r) {
+    constexpr int kPerWord = 4 / int(sizeof(typename Elem<XT>::T));
+    return swz<RS / kPerWord>(r) * kPerWord;
 }
 
 // Ordering of LDS accesses among the lanes of one wavefront.  A wavefront's LDS
@@ -56,38 +93,47 @@ __device__ __forceinline__ uint32_t div_f(uint32_t e, const Rows &in) {
     return in.n_features == 1 ? e : __umulhi(e, in.magic_f);
 }
 
+__device__ __forceinline__ uint32_t div_w(uint32_t e, const Rows &in) {
+    return in.n_words == 1 ? e : __umulhi(e, in.magic_w);
+}
+
 __device__ __forceinline__ int valid_rows(const Rows &in, int64_t tile) {
     const int64_t left = in.n - tile * kTileRows;
     return left < kTileRows ? int(left) : kTileRows;
 }
 
-// Store 4 consecutive features (c % 4 == 0) of row r into the swizzled tile.
-template <int RS>
+// Store 4 consecutive words (c % 4 == 0) of row r into the swizzled tile (rows of RSW
+// words; `tile` is the word view of the tile).
+template <int RSW>
 __device__ __forceinline__ void put4(float *tile, int r, int c, f32x4 v) {
-    float *row = tile + r * RS;
-    const int s = swz<RS>(r);
+    float *row = tile + r * RSW;
+    const int s = swz<RSW>(r);
     row[(c + 0) ^ s] = v.x;
     row[(c + 1) ^ s] = v.y;
     row[(c + 2) ^ s] = v.z;
     row[(c + 3) ^ s] = v.w;
 }
 
-// Vectorised staging (ld == F, F % 4 == 0, 16-byte aligned base), one tile held in
-// registers so that the next tile's loads overlap the walk of the current one.
+// Vectorised staging (dense rows of n_words 4-byte words, n_words % 4 == 0, 16-byte
+// aligned base), one tile held in registers so that the next tile's loads overlap the walk
+// of the current one.  RSW = LDS row stride in words.  The element type does not matter
+// here: words are moved unchanged.
 //
 // Loads are never guarded by a branch: guarded loads compile into branches whose joins
 // copy the loaded registers, which forces a wait for every outstanding load right after
 // the prefetch is issued.  A lane whose vector lies past the tile's valid data re-reads
 // the last valid vector instead, so rows past the end of the input hold copies of valid
-// features; their results are never stored.  EXACT (F == RS): every lane owns RS/4
-// vectors of a full tile and the LDS positions are shifts and masks.
-template <int RS, bool EXACT>
+// features; their results are never stored.  EXACT (n_words == RSW): every lane owns
+// RSW/4 vectors of a full tile and the LDS positions are shifts and masks.
+template <int RSW, bool EXACT>
 struct VecTile {
-    static constexpr int kVec = RS / 4;   // 16-byte vectors per lane for F == RS
+    static constexpr int kVec = RSW / 4;   // 16-byte vectors per lane for n_words == RSW
+    static_assert(kVec >= 1, "vector staging needs rows of at least 16 bytes");
     f32x4 v[kVec];
 
     __device__ __forceinline__ const f32x4 *base(const Rows &in, int64_t tile) const {
-        return reinterpret_cast<const f32x4 *>(in.x + tile * kTileRows * in.n_features);
+        return reinterpret_cast<const f32x4 *>(static_cast<const char *>(in.x) +
+                                               tile * kTileRows * in.n_words * 4);
     }
 
     // Any tile; nvec = vectors holding valid records (>= 1).
@@ -107,47 +153,48 @@ struct VecTile {
 #pragma unroll
             for (int k = 0; k < kVec; ++k) v[k] = __builtin_nontemporal_load(src + k * 64);
         } else {
-            load_clamped(in, tile, lane, kTileRows * in.n_features / 4);
+            load_clamped(in, tile, lane, kTileRows * in.n_words / 4);
         }
     }
 
     // Any tile, including the partial last one.
     __device__ __forceinline__ void load_tail(const Rows &in, int64_t tile, int lane) {
-        load_clamped(in, tile, lane, (valid_rows(in, tile) * in.n_features) >> 2);
+        load_clamped(in, tile, lane, (valid_rows(in, tile) * in.n_words) >> 2);
     }
 
     __device__ __forceinline__ void store(const Rows &in, float *tile, int lane) const {
         if constexpr (EXACT) {
-            constexpr int sh = __builtin_ctz(RS);
+            constexpr int sh = __builtin_ctz(RSW);
 #pragma unroll
             for (int k = 0; k < kVec; ++k) {
                 const int e = (k * 64 + lane) * 4;
-                put4<RS>(tile, e >> sh, e & (RS - 1), v[k]);
+                put4<RSW>(tile, e >> sh, e & (RSW - 1), v[k]);
             }
         } else {
-            const int full = kTileRows * in.n_features / 4;
+            const int full = kTileRows * in.n_words / 4;
 #pragma unroll
             for (int k = 0; k < kVec; ++k) {
                 const int q = k * 64 + lane;
                 if (q < full) {
                     const uint32_t e = uint32_t(q) * 4u;
-                    const int r = int(div_f(e, in));
-                    put4<RS>(tile, r, int(e) - r * in.n_features, v[k]);
+                    const int r = int(div_w(e, in));
+                    put4<RSW>(tile, r, int(e) - r * in.n_words, v[k]);
                 }
             }
         }
     }
 };
 
-// Vectorised staging of wide rows (RS > 64) in chunks of 16 vectors per lane, without
-// prefetch (loads clamped to the valid vectors as in VecTile).
-template <int RS>
+// Vectorised staging of wide rows (RSW > 64 words) in chunks of 16 vectors per lane,
+// without prefetch (loads clamped to the valid vectors as in VecTile).
+template <int RSW>
 __device__ __forceinline__ void stage_wide(const Rows &in, float *tile, int64_t t, int lane) {
-    const int nvec = (valid_rows(in, t) * in.n_features) >> 2;
-    const int full = kTileRows * in.n_features / 4;
-    const f32x4 *src = reinterpret_cast<const f32x4 *>(in.x + t * kTileRows * in.n_features);
+    const int nvec = (valid_rows(in, t) * in.n_words) >> 2;
+    const int full = kTileRows * in.n_words / 4;
+    const f32x4 *src = reinterpret_cast<const f32x4 *>(static_cast<const char *>(in.x) +
+                                                       t * kTileRows * in.n_words * 4);
 #pragma unroll 1
-    for (int k0 = 0; k0 < RS / 4; k0 += 16) {
+    for (int k0 = 0; k0 < RSW / 4; k0 += 16) {
         f32x4 v[16];
 #pragma unroll
         for (int k = 0; k < 16; ++k) {
@@ -159,39 +206,51 @@ __device__ __forceinline__ void stage_wide(const Rows &in, float *tile, int64_t 
             const int q = (k0 + k) * 64 + lane;
             if (q < full) {
                 const uint32_t e = uint32_t(q) * 4u;
-                const int r = int(div_f(e, in));
-                put4<RS>(tile, r, int(e) - r * in.n_features, v[k]);
+                const int r = int(div_w(e, in));
+                put4<RSW>(tile, r, int(e) - r * in.n_words, v[k]);
             }
         }
     }
 }
 
-// General staging: any ld >= F, any 4-byte alignment.
-template <int RS>
-__device__ __forceinline__ void stage_scalar(const Rows &in, float *tile, int64_t t, int lane) {
+// General staging: any ld >= F, element-aligned, one element per load.
+template <int XT, int RS>
+__device__ __forceinline__ void stage_scalar(const Rows &in, float *tile_words, int64_t t,
+                                             int lane) {
+    using T = typename Elem<XT>::T;
+    T *tile = reinterpret_cast<T *>(tile_words);
+    const T *x = static_cast<const T *>(in.x);
     const int64_t row0 = t * kTileRows;
     const int valid = valid_rows(in, t);
     for (int k = 0; k < in.n_features; ++k) {
         const uint32_t idx = uint32_t(k * 64 + lane);
         const int r = int(div_f(idx, in));
         const int c = int(idx) - r * in.n_features;
-        float v = 0.f;
-        if (r < valid) v = in.x[(row0 + r) * in.ld + c];
-        tile[r * RS + (c ^ swz<RS>(r))] = v;
+        T v = T(0);
+        if (r < valid) v = x[(row0 + r) * in.ld + c];
+        tile[r * RS + (c ^ swz_el<XT, RS>(r))] = v;
     }
 }
 
+// LDS row stride in words of a row of RS elements of XT, and whether the vector staging
+// path (16-byte loads, at least one vector per lane and row) exists for it.
+template <int XT, int RS>
+constexpr int row_words() { return RS * int(sizeof(typename Elem<XT>::T)) / 4; }
+template <int XT, int RS>
+constexpr bool has_vec_staging() { return row_words<XT, RS>() >= 4; }
+
 // Stage tile t without register prefetch.
-template <int RS, int LOAD>
+template <int XT, int RS, int LOAD>
 __device__ __forceinline__ void stage_now(const Rows &in, float *tile, int64_t t, int lane) {
-    if constexpr (LOAD != kLoadScalar && RS <= 64) {
-        VecTile<RS, LOAD == kLoadExact> buf;
+    constexpr int RSW = row_words<XT, RS>();
+    if constexpr (LOAD != kLoadScalar && has_vec_staging<XT, RS>() && RSW <= 64) {
+        VecTile<RSW, LOAD == kLoadExact> buf;
         buf.load_tail(in, t, lane);
         buf.store(in, tile, lane);
-    } else if constexpr (LOAD != kLoadScalar) {
-        stage_wide<RS>(in, tile, t, lane);
+    } else if constexpr (LOAD != kLoadScalar && has_vec_staging<XT, RS>()) {
+        stage_wide<RSW>(in, tile, t, lane);
     } else {
-        stage_scalar<RS>(in, tile, t, lane);
+        stage_scalar<XT, RS>(in, tile, t, lane);
     }
 }
 
@@ -201,8 +260,9 @@ __device__ __forceinline__ void stage_now(const Rows &in, float *tile, int64_t t
 // window or the result.  One-level lookahead: while node p's feature is read, both children
 // of p are fetched as one 16-byte pair and the comparison selects between them, so each
 // level costs one LDS round trip instead of two dependent ones.
+template <int XT>
 __device__ __forceinline__ int32_t walk_data(const Slot *slots, const int32_t *exits, int D,
-                                             int levels, const float *row, int sw) {
+                                             int levels, const typename Elem<XT>::T *row, int sw) {
     const int S = 1 << D;
     int w = 0;
     int32_t code = -1;
@@ -211,13 +271,13 @@ __device__ __forceinline__ int32_t walk_data(const Slot *slots, const int32_t *e
         int p = 1;
         Slot s = win[1];
         for (int k = 1; k < D; ++k) {
-            const float xv = row[s.f ^ sw];
+            const float xv = Elem<XT>::widen(row[s.f ^ sw]);
             const Slot2 kids = *reinterpret_cast<const Slot2 *>(win + 2 * p);
             const bool right = !(xv < s.t);
             p = 2 * p + int(right);
             s = right ? kids.r : kids.l;
         }
-        const float xv = row[s.f ^ sw];
+        const float xv = Elem<XT>::widen(row[s.f ^ sw]);
         p = 2 * p + int(!(xv < s.t));
         code = exits[(w << D) + p - S];
         if (code < 0) break;
@@ -281,8 +341,9 @@ __device__ __forceinline__ void walk_data_k(const char *const (&base)[K], const 
 // wavefront instruction evaluates 64/S records' windows.  One ballot gathers the 64
 // outcomes; record r's segment is handed to lane r, which walks its bits from the window
 // root to the exit.
-template <int RS, int D>
+template <int XT, int RS, int D>
 struct Spec {
+    using T = typename Elem<XT>::T;
     static constexpr int S = 1 << D;
     using Bits = typename std::conditional<(S > 32), uint64_t, uint32_t>::type;
     int j;          // slot evaluated by this lane (slot 0 is padding)
@@ -295,7 +356,7 @@ struct Spec {
     // evaluates record b + g, so record r's bits arrive in r's own segment in the round
     // g == r % S.
     __device__ __forceinline__ Bits eval(const Slot *slots, bool first, const Slot &root, int w,
-                                         const float *tile) const {
+                                         const T *tile) const {
         Bits bits = 0;
 #pragma unroll 8
         for (int g = 0; g < S; ++g) {
@@ -311,7 +372,7 @@ struct Spec {
                     wr = __shfl(w, r);
                 p = slots[(wr << D) + j];
             }
-            const float xv = tile[r * RS + (p.f ^ swz<RS>(r))];
+            const float xv = Elem<XT>::widen(tile[r * RS + (p.f ^ swz_el<XT, RS>(r))]);
             const uint64_t m = __ballot(!(xv < p.t));
             if (j == g) bits = Bits(m >> seg_shift);
         }
@@ -329,7 +390,7 @@ struct Spec {
     // Exit code of every lane's record.  `root` = slots[j] of window 0.  All 64 lanes
     // must be active.
     __device__ __forceinline__ int32_t run(const Slot *slots, const int32_t *exits, int levels,
-                                           const Slot &root, const float *tile) const {
+                                           const Slot &root, const T *tile) const {
         int w = 0;
         int32_t code = exits[walk(eval(slots, true, root, 0, tile))];
         bool done = code < 0;
@@ -402,9 +463,10 @@ __device__ __forceinline__ void flush_results(const KArgs &a, const uint8_t *buf
 // of the output.  `body(t)` walks staged tile t and returns each lane's result.  No
 // workgroup barrier inside: the wavefronts of a workgroup process different numbers of
 // tiles.
-template <int RS, int LOAD, class Body>
+template <int XT, int RS, int LOAD, class Body>
 __device__ __forceinline__ void tile_loop(const KArgs &a, float *tile, uint8_t *obuf, int lane,
                                           Body body) {
+    constexpr int RSW = row_words<XT, RS>();
     const int64_t G = int64_t(gridDim.x) * a.waves;
     const int64_t gw = int64_t(blockIdx.x) * a.waves + (threadIdx.x >> 6);
     const int64_t chunk = (a.in.n_tiles + G - 1) / G;
@@ -428,10 +490,10 @@ __device__ __forceinline__ void tile_loop(const KArgs &a, float *tile, uint8_t *
         }
     };
 
-    if constexpr (LOAD != kLoadScalar && RS <= 64) {
+    if constexpr (LOAD != kLoadScalar && has_vec_staging<XT, RS>() && RSW <= 64) {
         // Full tiles: the loads of tile t + 1 are in flight in registers while tile t is
         // walked.  The partial last tile of the input, if any, is staged on its own.
-        VecTile<RS, LOAD == kLoadExact> buf;
+        VecTile<RSW, LOAD == kLoadExact> buf;
         const int64_t tf = t1 < n_full ? t1 : n_full;
         int64_t t = t0;
         if (t < tf) buf.load_full(a.in, t, lane);
@@ -444,14 +506,14 @@ __device__ __forceinline__ void tile_loop(const KArgs &a, float *tile, uint8_t *
         }
         if (t < t1) {                         // t == n_full: the partial tile
             wave_sync();
-            stage_now<RS, LOAD>(a.in, tile, t, lane);
+            stage_now<XT, RS, LOAD>(a.in, tile, t, lane);
             wave_sync();
             finish(t, body(t));
         }
     } else {
         for (int64_t t = t0; t < t1; ++t) {
             wave_sync();
-            stage_now<RS, LOAD>(a.in, tile, t, lane);
+            stage_now<XT, RS, LOAD>(a.in, tile, t, lane);
             wave_sync();
             finish(t, body(t));
         }
@@ -459,14 +521,15 @@ __device__ __forceinline__ void tile_loop(const KArgs &a, float *tile, uint8_t *
 }
 
 // LDS layout: [tables (if staged)] [one record tile per wavefront] [one result buffer per
-// wavefront].
-template <int RS>
+// wavefront].  `tile` is the word view of this wavefront's tile.
+template <int XT, int RS>
 __device__ __forceinline__ void wave_buffers(const KArgs &a, char *after_tables, float *&tile,
                                              uint8_t *&obuf) {
+    constexpr int kTileBytes = kTileRows * row_words<XT, RS>() * 4;
     const int wave = threadIdx.x >> 6;
-    tile = reinterpret_cast<float *>(after_tables) + wave * (kTileRows * RS);
+    tile = reinterpret_cast<float *>(after_tables + wave * kTileBytes);
     const int obytes = out_buffer_bytes(a.out_cap, a.out_kind == 0 ? 1 : 4);
-    obuf = reinterpret_cast<uint8_t *>(after_tables) + a.waves * (kTileRows * RS * 4) + wave * obytes;
+    obuf = reinterpret_cast<uint8_t *>(after_tables) + a.waves * kTileBytes + wave * obytes;
 }
 
 template <class T>

@@ -170,9 +170,8 @@ std::vector<const void *> g_prepared;
 // add contention.  The speculative decomposition, which does 2^D times the lane work per
 // record, runs best with 8 wavefronts per CU on every tile width (fewer leave its LDS
 // latency exposed, more slow it down).
-int target_waves_per_cu(int algo, int row_stride) {
+int target_waves_per_cu(int algo, int tile_bytes) {
     if (algo != DT_ALGO_DATA) return 8;
-    const int tile_bytes = dtree::kTileRows * row_stride * 4;
     return std::max(2, std::min(32, (64 * 1024) / tile_bytes));
 }
 
@@ -194,12 +193,15 @@ constexpr int kMinLdsWaves = 2;
 constexpr int kMaxOutCap = 256;
 
 // Single-tree plan: workgroup shape, resident workgroups per CU and the result buffer, for
-// results of `out_bytes` bytes (1 or 4).  The path kernel also keeps its path arrays
-// (kPathIntsPerWave ints per wavefront) after the result buffers.
-dt_status make_plan(const DeviceCaps &caps, int algo, int row_stride, int load_mode, int depth,
-                    int64_t table_bytes, int out_bytes, int waves_per_cu, Plan *plan) {
+// records of element type `elem_type` and results of `out_bytes` bytes (1 or 4).  The path
+// kernel also keeps its path arrays (kPathIntsPerWave ints per wavefront) after the result
+// buffers.
+dt_status make_plan(const DeviceCaps &caps, int algo, int elem_type, int row_stride,
+                    int load_mode, int depth, int64_t table_bytes, int out_bytes,
+                    int waves_per_cu, Plan *plan) {
     const int path_bytes = algo == DT_ALGO_PATH ? dtree::kPathIntsPerWave * 4 : 0;
-    const int tile_bytes = dtree::kTileRows * row_stride * 4 + path_bytes;
+    const int record_tile_bytes = dtree::tile_bytes_for(row_stride, elem_type);
+    const int tile_bytes = record_tile_bytes + path_bytes;
     const int res_bytes = dtree::kTileRows * out_bytes;   // one tile of results
     if (tile_bytes + res_bytes > caps.lds_per_block) {
         plan->why = "one record tile exceeds the workgroup LDS";
@@ -209,7 +211,7 @@ dt_status make_plan(const DeviceCaps &caps, int algo, int row_stride, int load_m
         table_bytes + int64_t(kMinLdsWaves) * (tile_bytes + res_bytes) <= caps.lds_per_block;
     const int table_lds = tab_lds ? int(table_bytes) : 0;
     plan->tables_in_lds = tab_lds ? 1 : 0;
-    plan->fn = dtree::kernel_for(algo, row_stride, load_mode, tab_lds, depth);
+    plan->fn = dtree::kernel_for(algo, elem_type, row_stride, load_mode, tab_lds, depth);
     if (!plan->fn) {
         plan->why = "no kernel instance for this configuration";
         return plan->status = DT_ERR_UNSUPPORTED;
@@ -218,7 +220,8 @@ dt_status make_plan(const DeviceCaps &caps, int algo, int row_stride, int load_m
     prepare_once(plan->fn, caps.lds_per_block, plan);
     if (plan->status != DT_OK) return plan->status;
 
-    const int target = waves_per_cu > 0 ? waves_per_cu : target_waves_per_cu(algo, row_stride);
+    const int target =
+        waves_per_cu > 0 ? waves_per_cu : target_waves_per_cu(algo, record_tile_bytes);
     // Try every workgroup size and count per CU; keep the shape reaching the most resident
     // wavefronts up to the target (registers and the LDS both limit residency); on ties
     // prefer larger workgroups (fewer table copies), then a larger result buffer.
@@ -229,8 +232,8 @@ dt_status make_plan(const DeviceCaps &caps, int algo, int row_stride, int load_m
             if (table_lds + w * (tile_bytes + res_bytes) > budget) continue;
             const int cap =
                 std::min(kMaxOutCap, (budget - table_lds - w * tile_bytes) / (w * res_bytes));
-            const int lds =
-                dtree::lds_bytes_for(table_lds, row_stride, w, cap * res_bytes) + w * path_bytes;
+            const int lds = dtree::lds_bytes_for(table_lds, record_tile_bytes, w, cap * res_bytes) +
+                            w * path_bytes;
             int nb = 0;
             hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, plan->fn, w * 64,
                                                                         size_t(lds));
@@ -268,7 +271,8 @@ struct dt_tree {
     int row_stride = 0;
     int path_hops = kDefaultPathHops;
     Encoding enc[2];              // data windows, speculative windows (also the path kernel's)
-    Plan plan[3][dtree::kLoadModes][2];   // [algo][load mode][uint8 / int32 results]
+    // [algo][record element type][load mode][uint8 / int32 results]
+    Plan plan[3][dtree::kElemTypes][dtree::kLoadModes][2];
 };
 
 // Encoding an algorithm runs on: the path kernel reduces the speculative windows.
@@ -315,31 +319,41 @@ struct dt_forest {
 namespace {
 
 // The fastest record-tile load path the layout of the features allows.
-int load_mode_for(const float *d_x, int64_t ld, int32_t n_features, int row_stride) {
-    const bool dense = ld == n_features && n_features % 4 == 0 &&
+int load_mode_for(const void *d_x, int elem_type, int64_t ld, int32_t n_features,
+                  int row_stride) {
+    const bool dense = ld == n_features && (n_features * dtree::elem_bytes(elem_type)) % 16 == 0 &&
                        (reinterpret_cast<uintptr_t>(d_x) & 15u) == 0;
     if (!dense) return dtree::kLoadScalar;
     return n_features == row_stride ? dtree::kLoadExact : dtree::kLoadVec;
 }
 
-dtree::Rows make_rows(const float *d_x, int64_t n, int64_t ld, int32_t n_features) {
+uint32_t magic_div(int32_t d) {
+    return d >= 2 ? uint32_t(((uint64_t(1) << 32) + uint64_t(d) - 1) / uint64_t(d)) : 0u;
+}
+
+dtree::Rows make_rows(const void *d_x, int elem_type, int64_t n, int64_t ld, int32_t n_features) {
     dtree::Rows r{};
     r.x = d_x;
     r.n = n;
     r.ld = ld;
     r.n_tiles = (n + dtree::kTileRows - 1) / dtree::kTileRows;
     r.n_features = n_features;
-    r.magic_f = n_features >= 2 ? uint32_t(((uint64_t(1) << 32) + uint64_t(n_features) - 1) /
-                                           uint64_t(n_features))
-                                : 0u;
+    r.magic_f = magic_div(n_features);
+    r.n_words = n_features * dtree::elem_bytes(elem_type) / 4;   // used by vector loads only
+    r.magic_w = magic_div(r.n_words);
     return r;
 }
 
-dt_status classify_impl(const dt_tree *tree, const float *d_x, int64_t n, int64_t ld,
-                        void *d_out, dt_output out_kind, dt_algo algo, void *stream) {
+bool valid_elem_type(dt_dtype t) {
+    return t == DT_F32 || t == DT_F16 || t == DT_BF16 || t == DT_U8;
+}
+
+dt_status classify_impl(const dt_tree *tree, const void *d_x, dt_dtype x_type, int64_t n,
+                        int64_t ld, void *d_out, dt_output out_kind, dt_algo algo, void *stream) {
     if (!tree) return fail(DT_ERR_INVALID_ARG, "tree is NULL");
     if (n < 0) return fail(DT_ERR_INVALID_ARG, "n must be >= 0");
     if (!single_tree_algo(algo)) return fail(DT_ERR_INVALID_ARG, "unknown algo");
+    if (!valid_elem_type(x_type)) return fail(DT_ERR_INVALID_ARG, "unknown x_type");
     if (out_kind != DT_OUT_CLASS_U8 && out_kind != DT_OUT_CLASS_I32 &&
         out_kind != DT_OUT_LEAF_I32)
         return fail(DT_ERR_INVALID_ARG, "unknown out_kind");
@@ -357,13 +371,15 @@ dt_status classify_impl(const dt_tree *tree, const float *d_x, int64_t n, int64_
     if (dev != tree->caps.device)
         return fail(DT_ERR_INVALID_ARG, "current device differs from the tree's device");
 
-    const Plan &plan = tree->plan[algo][load_mode_for(d_x, ld, tree->n_features, tree->row_stride)]
-                                 [out_kind == DT_OUT_CLASS_U8 ? 0 : 1];
+    if ((reinterpret_cast<uintptr_t>(d_x) % uintptr_t(dtree::elem_bytes(x_type))) != 0)
+        return fail(DT_ERR_INVALID_ARG, "d_x is not aligned to its element size");
+    const int mode = load_mode_for(d_x, x_type, ld, tree->n_features, tree->row_stride);
+    const Plan &plan = tree->plan[algo][x_type][mode][out_kind == DT_OUT_CLASS_U8 ? 0 : 1];
     if (plan.status != DT_OK) return fail(plan.status, plan.why);
     const Encoding &enc = tree->enc[encoding_of(algo)];
 
     dtree::KArgs a{};
-    a.in = make_rows(d_x, n, ld, tree->n_features);
+    a.in = make_rows(d_x, x_type, n, ld, tree->n_features);
     a.slots = enc.d_slots;
     a.exits = out_kind == DT_OUT_LEAF_I32 ? enc.d_exit_leaf : enc.d_exit_class;
     a.slot_bytes = int32_t(enc.slot_bytes);
@@ -418,16 +434,24 @@ dt_status create_impl(const dt_node *nodes, int32_t n_nodes, int32_t n_features,
     }
     for (int algo = 0; algo < 3; ++algo) {
         const Encoding &enc = t->enc[encoding_of(algo)];
-        for (int m = 0; m < dtree::kLoadModes; ++m) {
-            if (t->row_stride > dtree::kMaxRowStride) {
-                t->plan[algo][m][0].why = t->plan[algo][m][1].why = "n_features > 256";
-                continue;
+        for (int xt = 0; xt < dtree::kElemTypes; ++xt) {
+            for (int m = 0; m < dtree::kLoadModes; ++m) {
+                Plan *pl = t->plan[algo][xt][m];
+                if (t->row_stride > dtree::kMaxRowStride) {
+                    pl[0].why = pl[1].why = "n_features > 256";
+                    continue;
+                }
+                if (algo == DT_ALGO_PATH && xt != DT_F32) {
+                    pl[0].why = pl[1].why = "the path kernel reads fp32 records only";
+                    continue;
+                }
+                if (m == dtree::kLoadExact && n_features != t->row_stride) continue;
+                if (m != dtree::kLoadScalar && (n_features * dtree::elem_bytes(xt)) % 16 != 0)
+                    continue;
+                for (int o = 0; o < 2; ++o)
+                    make_plan(t->caps, algo, xt, t->row_stride, m, enc.depth, enc.table_bytes(),
+                              o == 0 ? 1 : 4, opt ? opt->waves_per_cu : 0, &pl[o]);
             }
-            if (m == dtree::kLoadExact && n_features != t->row_stride) continue;
-            if (m != dtree::kLoadScalar && n_features % 4 != 0) continue;
-            for (int o = 0; o < 2; ++o)
-                make_plan(t->caps, algo, t->row_stride, m, enc.depth, enc.table_bytes(),
-                          o == 0 ? 1 : 4, opt ? opt->waves_per_cu : 0, &t->plan[algo][m][o]);
         }
     }
     *out = t;
@@ -480,7 +504,7 @@ void encode_forest(const dt_node *nodes, const int32_t *offsets, int32_t n_trees
 
 // Choose the workgroup shape and the LDS chunks of consecutive trees.
 void chunk_forest(const DeviceCaps &caps, int row_stride, ForestEncoding *enc) {
-    const int64_t tile_bytes = int64_t(dtree::kTileRows) * row_stride * 4;
+    const int64_t tile_bytes = dtree::tile_bytes_for(row_stride, dtree::kXF32);
     enc->chunks.clear();
     for (int w = dtree::kMaxWavesPerBlock; w >= 1; --w) {
         const int64_t budget = int64_t(caps.lds_per_block) - w * tile_bytes;
@@ -559,7 +583,8 @@ dt_status plan_forest(const DeviceCaps &caps, int algo, int row_stride, int load
     int best_waves = 0;
     for (int w = 1; w <= dtree::kMaxWavesPerBlock; ++w) {
         if (tab_lds && w != enc.waves) continue;     // the chunks were cut for enc.waves
-        const int lds = dtree::lds_bytes_for(enc.chunk_lds_bytes, row_stride, w);
+        const int lds = dtree::lds_bytes_for(enc.chunk_lds_bytes,
+                                             dtree::tile_bytes_for(row_stride, dtree::kXF32), w);
         if (lds > caps.lds_per_block) break;
         int nb = 0;
         hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, plan->fn, w * 64,
@@ -691,12 +716,13 @@ dt_status forest_classify_impl(const dt_forest *f, const float *d_x, int64_t n, 
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
     if (dev != f->caps.device)
         return fail(DT_ERR_INVALID_ARG, "current device differs from the forest's device");
-    const Plan &plan = f->plan[algo][load_mode_for(d_x, ld, f->n_features, f->row_stride)];
+    const Plan &plan =
+        f->plan[algo][load_mode_for(d_x, dtree::kXF32, ld, f->n_features, f->row_stride)];
     if (plan.status != DT_OK) return fail(plan.status, plan.why);
     const ForestEncoding &enc = f->enc[algo];
 
     dtree::FArgs a{};
-    a.in = make_rows(d_x, n, ld, f->n_features);
+    a.in = make_rows(d_x, dtree::kXF32, n, ld, f->n_features);
     a.tables = enc.d_tables;
     a.trees = enc.d_trees;
     a.chunks = enc.d_chunks;
@@ -832,16 +858,17 @@ dt_status dt_tree_get_info(const dt_tree *t, dt_tree_info *info) {
 
 void dt_tree_destroy(dt_tree *t) { destroy_impl(t); }
 
-dt_status dt_tree_launch_info(const dt_tree *t, const float *d_x, int64_t ld, dt_output out_kind,
-                              dt_algo algo, dt_launch_info *info) {
+dt_status dt_tree_launch_info(const dt_tree *t, const void *d_x, dt_dtype x_type, int64_t ld,
+                              dt_output out_kind, dt_algo algo, dt_launch_info *info) {
     g_last_error.clear();
     if (!t || !info) return fail(DT_ERR_INVALID_ARG, "null argument");
     if (!single_tree_algo(algo)) return fail(DT_ERR_INVALID_ARG, "unknown algo");
+    if (!valid_elem_type(x_type)) return fail(DT_ERR_INVALID_ARG, "unknown x_type");
     if (out_kind != DT_OUT_CLASS_U8 && out_kind != DT_OUT_CLASS_I32 && out_kind != DT_OUT_LEAF_I32)
         return fail(DT_ERR_INVALID_ARG, "unknown out_kind");
     if (ld < t->n_features) return fail(DT_ERR_INVALID_ARG, "ld must be >= n_features");
-    const int mode = load_mode_for(d_x, ld, t->n_features, t->row_stride);
-    const Plan &plan = t->plan[algo][mode][out_kind == DT_OUT_CLASS_U8 ? 0 : 1];
+    const int mode = load_mode_for(d_x, x_type, ld, t->n_features, t->row_stride);
+    const Plan &plan = t->plan[algo][x_type][mode][out_kind == DT_OUT_CLASS_U8 ? 0 : 1];
     if (plan.status != DT_OK) return fail(plan.status, plan.why);
     info->waves_per_workgroup = plan.waves;
     info->workgroups_per_cu = plan.blocks_per_cu;
@@ -856,7 +883,18 @@ dt_status dt_classify(const dt_tree *t, const float *d_x, int64_t n, int64_t ld,
                       dt_output out_kind, dt_algo algo, void *stream) {
     try {
         g_last_error.clear();
-        return classify_impl(t, d_x, n, ld, d_out, out_kind, algo, stream);
+        return classify_impl(t, d_x, DT_F32, n, ld, d_out, out_kind, algo, stream);
+    } catch (...) {
+        return fail(DT_ERR_INVALID_ARG, "unexpected internal error");
+    }
+}
+
+dt_status dt_classify_typed(const dt_tree *t, const void *d_x, dt_dtype x_type, int64_t n,
+                            int64_t ld, void *d_out, dt_output out_kind, dt_algo algo,
+                            void *stream) {
+    try {
+        g_last_error.clear();
+        return classify_impl(t, d_x, x_type, n, ld, d_out, out_kind, algo, stream);
     } catch (...) {
         return fail(DT_ERR_INVALID_ARG, "unexpected internal error");
     }

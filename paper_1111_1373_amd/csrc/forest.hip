@@ -67,9 +67,9 @@ __global__ void __launch_bounds__(512) forest_kernel(FArgs a) {
         const Slot *sl = reinterpret_cast<const Slot *>(base);
         const int32_t *ex = reinterpret_cast<const int32_t *>(base + slot_bytes);
         if constexpr (SD == 0) {
-            return dev::walk_data(sl, ex, a.depth, levels, row, sw);
+            return dev::walk_data<kXF32>(sl, ex, a.depth, levels, row, sw);
         } else {
-            const dev::Spec<RS, SD> spec(lane);
+            const dev::Spec<kXF32, RS, SD> spec(lane);
             const Slot root = sl[spec.j];
             return spec.run(sl, ex, levels, root, tile);
         }
@@ -91,7 +91,7 @@ __global__ void __launch_bounds__(512) forest_kernel(FArgs a) {
             if (kPrefetch && t < n_full)
                 buf.store(a.in, tile, lane);
             else
-                dev::stage_now<RS, LOAD>(a.in, tile, t, lane);
+                dev::stage_now<kXF32, RS, LOAD>(a.in, tile, t, lane);
         }
         dev::wave_sync();
         if constexpr (kPrefetch) {

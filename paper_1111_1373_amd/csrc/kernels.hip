@@ -1,106 +1,23 @@
-// gfx950 kernels for single-tree evaluation.
-//
-// Both kernels are persistent: each wavefront owns a private tile of 64 records in the
-// LDS and walks a contiguous range of record tiles, keeping the loads of its next tile in
-// flight in registers while it walks the current one, and writing its results in bursts
-// from an LDS buffer.  The tree's window tables
-// (see encode.hpp) are staged into the LDS once per workgroup, or, for trees whose tables
-// do not fit next to the record tiles, read from global memory (L2-resident).
-//
-//   data_kernel  (Section 3.2, Procedure 3): lane r evaluates record r of its tile.
-//   spec_kernel  (Sections 3.3-3.4, Procedures 4-5): 2^D lanes evaluate all slots of a
-//                record's current window at once; a wavefront ballot gathers the outcomes
-//                and the exit is found by walking the bits.  The mask replaces the paper's
-//                shared `path` array and its barrier-separated pointer jumping.
-#include "device_common.hpp"
+// Single-tree kernels for fp32 records, and the dispatch over element types, load modes and
+// algorithms (kernel templates in kernels_impl.hpp).
+#include "kernels_impl.hpp"
 
 namespace dtree {
-namespace {
 
-using dev::Slot;
-
-template <int RS, int LOAD, bool TAB_LDS>
-__global__ void __launch_bounds__(512) data_kernel(KArgs a) {
-    extern __shared__ int4 lds[];
-    const Slot *slots;
-    const int32_t *exits;
-    char *tiles = dev::bind_tables<TAB_LDS>(a, lds, slots, exits);
-    const int lane = threadIdx.x & 63;
-    float *tile;
-    uint8_t *obuf;
-    dev::wave_buffers<RS>(a, tiles, tile, obuf);
-    const float *row = tile + lane * RS;
-    const int sw = dev::swz<RS>(lane);
-    dev::tile_loop<RS, LOAD>(a, tile, obuf, lane, [&](int64_t) -> int32_t {
-        return ~dev::walk_data(slots, exits, a.depth, a.levels, row, sw);
-    });
+const void *kernel_for_f32(int algo, int row_stride, int load_mode, bool tables_in_lds, int depth) {
+    return single_tree_kernel<kXF32>(algo, row_stride, load_mode, tables_in_lds, depth);
 }
 
-template <int RS, int LOAD, bool TAB_LDS, int D>
-__global__ void __launch_bounds__(512) spec_kernel(KArgs a) {
-    extern __shared__ int4 lds[];
-    const Slot *slots;
-    const int32_t *exits;
-    char *tiles = dev::bind_tables<TAB_LDS>(a, lds, slots, exits);
-    const int lane = threadIdx.x & 63;
-    float *tile;
-    uint8_t *obuf;
-    dev::wave_buffers<RS>(a, tiles, tile, obuf);
-    const dev::Spec<RS, D> spec(lane);
-    const Slot root = slots[spec.j];   // window 0 is shared by every record
-    dev::tile_loop<RS, LOAD>(a, tile, obuf, lane, [&](int64_t) -> int32_t {
-        return ~spec.run(slots, exits, a.levels, root, tile);
-    });
-}
-
-// ---- instance tables ------------------------------------------------------------------
-template <int RS, int LOAD, bool TAB_LDS>
-const void *spec_for(int depth) {
-    switch (depth) {
-        case 1: return reinterpret_cast<const void *>(&spec_kernel<RS, LOAD, TAB_LDS, 1>);
-        case 2: return reinterpret_cast<const void *>(&spec_kernel<RS, LOAD, TAB_LDS, 2>);
-        case 3: return reinterpret_cast<const void *>(&spec_kernel<RS, LOAD, TAB_LDS, 3>);
-        case 4: return reinterpret_cast<const void *>(&spec_kernel<RS, LOAD, TAB_LDS, 4>);
-        case 5: return reinterpret_cast<const void *>(&spec_kernel<RS, LOAD, TAB_LDS, 5>);
-        case 6: return reinterpret_cast<const void *>(&spec_kernel<RS, LOAD, TAB_LDS, 6>);
-        default: return nullptr;
-    }
-}
-
-template <int RS, int LOAD, bool TAB_LDS>
-const void *for_variant(int algo, int depth) {
-    if (algo == kAlgoData) return reinterpret_cast<const void *>(&data_kernel<RS, LOAD, TAB_LDS>);
-    return spec_for<RS, LOAD, TAB_LDS>(depth);
-}
-
-template <int RS, int LOAD>
-const void *for_load(int algo, bool tab_lds, int depth) {
-    return tab_lds ? for_variant<RS, LOAD, true>(algo, depth)
-                   : for_variant<RS, LOAD, false>(algo, depth);
-}
-
-template <int RS>
-const void *for_stride(int algo, int load_mode, bool tab_lds, int depth) {
-    switch (load_mode) {
-        case kLoadScalar: return for_load<RS, kLoadScalar>(algo, tab_lds, depth);
-        case kLoadVec: return for_load<RS, kLoadVec>(algo, tab_lds, depth);
-        case kLoadExact: return for_load<RS, kLoadExact>(algo, tab_lds, depth);
-        default: return nullptr;
-    }
-}
-
-}  // namespace
-
-const void *kernel_for(int algo, int row_stride, int load_mode, bool tables_in_lds, int depth) {
-    if (algo == kAlgoPath) return path_kernel_for(row_stride, load_mode, tables_in_lds, depth);
-    switch (row_stride) {
-        case 4: return for_stride<4>(algo, load_mode, tables_in_lds, depth);
-        case 8: return for_stride<8>(algo, load_mode, tables_in_lds, depth);
-        case 16: return for_stride<16>(algo, load_mode, tables_in_lds, depth);
-        case 32: return for_stride<32>(algo, load_mode, tables_in_lds, depth);
-        case 64: return for_stride<64>(algo, load_mode, tables_in_lds, depth);
-        case 128: return for_stride<128>(algo, load_mode, tables_in_lds, depth);
-        case 256: return for_stride<256>(algo, load_mode, tables_in_lds, depth);
+const void *kernel_for(int algo, int elem_type, int row_stride, int load_mode, bool tables_in_lds,
+                       int depth) {
+    if (algo == kAlgoPath)
+        return elem_type == kXF32 ? path_kernel_for(row_stride, load_mode, tables_in_lds, depth)
+                                  : nullptr;
+    switch (elem_type) {
+        case kXF32: return kernel_for_f32(algo, row_stride, load_mode, tables_in_lds, depth);
+        case kXF16: return kernel_for_f16(algo, row_stride, load_mode, tables_in_lds, depth);
+        case kXBF16: return kernel_for_bf16(algo, row_stride, load_mode, tables_in_lds, depth);
+        case kXU8: return kernel_for_u8(algo, row_stride, load_mode, tables_in_lds, depth);
         default: return nullptr;
     }
 }

@@ -13,14 +13,21 @@ constexpr int kMaxWavesPerBlock = 8;   // kernels are built for <= 512 threads
 constexpr int kMaxForestTrees = 255;   // 8-bit vote counters
 constexpr int kMaxForestClasses = 64;  // 16 VGPRs of packed counters
 
+// Record element types (values of dt_dtype).  Each widens exactly to fp32.
+enum ElemType { kXF32 = 0, kXF16 = 1, kXBF16 = 2, kXU8 = 3, kElemTypes = 4 };
+
+__host__ __device__ inline int elem_bytes(int xt) { return xt == kXF32 ? 4 : xt == kXU8 ? 1 : 2; }
+
 // The record matrix a kernel reads.
 struct Rows {
-    const float *x;          // device features, row-major
+    const void *x;           // device records, row-major, elements of the kernel's type
     int64_t n;               // records
-    int64_t ld;              // row stride in floats
+    int64_t ld;              // row stride in elements
     int64_t n_tiles;         // ceil(n / 64)
     int32_t n_features;      // F
     uint32_t magic_f;        // ceil(2^32 / F) for F >= 2 (row = idx / F via mulhi)
+    int32_t n_words;         // 4-byte words per dense row, F * elem_bytes / 4 (vector loads)
+    uint32_t magic_w;        // ceil(2^32 / n_words) for n_words >= 2
 };
 
 // Single-tree kernel arguments (passed by value).
@@ -69,19 +76,26 @@ enum KernelAlgo { kAlgoData = 0, kAlgoSpec = 1, kAlgoPath = 2 };
 
 // How record tiles are read from HBM.
 enum LoadMode {
-    kLoadScalar = 0,   // any ld >= F, 4-byte aligned: one float per load
-    kLoadVec = 1,      // ld == F, F % 4 == 0, 16-byte aligned base: 16-byte loads
-    kLoadExact = 2,    // as kLoadVec and F == the LDS row stride: every lane loads RS/4
-                       // vectors per tile with no bounds test
+    kLoadScalar = 0,   // any ld >= F, element-aligned: one element per load
+    kLoadVec = 1,      // ld == F, F * elem_bytes % 16 == 0, 16-byte aligned base: 16-byte loads
+    kLoadExact = 2,    // as kLoadVec and F == the LDS row stride: every lane loads the same
+                       // number of vectors per tile with no bounds test
     kLoadModes = 3
 };
 
-// Kernel instance for (algorithm, LDS row stride, load mode, tables staged in the LDS or
-// read from global memory, window depth), or nullptr if no such instance exists.
-// `depth` is ignored by the data kernel.
-const void *kernel_for(int algo, int row_stride, int load_mode, bool tables_in_lds, int depth);
+// Kernel instance for (algorithm, record element type, LDS row stride in elements, load
+// mode, tables staged in the LDS or read from global memory, window depth), or nullptr if
+// no such instance exists.  `depth` is ignored by the data kernel.
+const void *kernel_for(int algo, int elem_type, int row_stride, int load_mode, bool tables_in_lds,
+                       int depth);
 
-// Path-reduction kernel instance (speculative windows of depth 1..6).
+// Per element type (one translation unit each): data and speculative kernel instances.
+const void *kernel_for_f32(int algo, int row_stride, int load_mode, bool tables_in_lds, int depth);
+const void *kernel_for_f16(int algo, int row_stride, int load_mode, bool tables_in_lds, int depth);
+const void *kernel_for_bf16(int algo, int row_stride, int load_mode, bool tables_in_lds, int depth);
+const void *kernel_for_u8(int algo, int row_stride, int load_mode, bool tables_in_lds, int depth);
+
+// Path-reduction kernel instance (fp32 records, speculative windows of depth 1..6).
 const void *path_kernel_for(int row_stride, int load_mode, bool tables_in_lds, int depth);
 
 // Forest kernel instance; `vote_words` = 32-bit words of packed 8-bit counters
@@ -98,10 +112,15 @@ hipError_t launch_kernel(const void *fn, const KArgs &args, int blocks, int lds_
 hipError_t launch_forest(const void *fn, const FArgs &args, int blocks, int lds_bytes,
                          hipStream_t stream);
 
+// LDS bytes of one record tile: 64 rows of `row_stride` elements of `elem_type`.
+inline int tile_bytes_for(int row_stride, int elem_type) {
+    return kTileRows * row_stride * elem_bytes(elem_type);
+}
+
 // Dynamic LDS of a workgroup of `waves` wavefronts: tables, one record tile per wavefront,
 // then (single-tree kernels) one result buffer of `out_bytes_per_wave` per wavefront.
-inline int lds_bytes_for(int table_bytes, int row_stride, int waves, int out_bytes_per_wave = 0) {
-    return table_bytes + waves * (kTileRows * row_stride * 4 + out_bytes_per_wave);
+inline int lds_bytes_for(int table_bytes, int tile_bytes, int waves, int out_bytes_per_wave = 0) {
+    return table_bytes + waves * (tile_bytes + out_bytes_per_wave);
 }
 
 }  // namespace dtree

@@ -104,7 +104,7 @@ __global__ void __launch_bounds__(512) path_kernel(KArgs a) {
     const int lane = threadIdx.x & 63;
     float *tile;
     uint8_t *obuf;
-    dev::wave_buffers<RS>(a, tiles, tile, obuf);
+    dev::wave_buffers<kXF32, RS>(a, tiles, tile, obuf);
     // path arrays follow the result buffers: one int per lane pair (2S per segment)
     int *wave_path = reinterpret_cast<int *>(
                          tiles + a.waves * (kTileRows * RS * 4 +
@@ -112,7 +112,7 @@ __global__ void __launch_bounds__(512) path_kernel(KArgs a) {
                      (threadIdx.x >> 6) * kPathIntsPerWave;
     const PathJump<RS, D> pj(lane, wave_path);
     const Slot root = slots[pj.j];
-    dev::tile_loop<RS, LOAD>(a, tile, obuf, lane, [&](int64_t) -> int32_t {
+    dev::tile_loop<kXF32, RS, LOAD>(a, tile, obuf, lane, [&](int64_t) -> int32_t {
         return ~pj.run(slots, exits, a.levels, root, tile, a.hops);
     });
 }

@@ -31,6 +31,7 @@ _lib = ctypes.CDLL(LIB_PATH)
 DT_OK, DT_ERR_INVALID_ARG, DT_ERR_INVALID_TREE, DT_ERR_UNSUPPORTED, DT_ERR_HIP, DT_ERR_NO_MEMORY = range(6)
 ALGOS = {"data": 0, "speculative": 1, "path": 2}
 OUT_KINDS = {"class_u8": 0, "class_i32": 1, "leaf_i32": 2}
+X_TYPES = {"f32": 0, "f16": 1, "bf16": 2, "u8": 3}
 
 NODE_DTYPE = np.dtype(
     [("feature", "<i4"), ("threshold", "<f4"), ("left", "<i4"), ("cls", "<i4")], align=False)
@@ -86,8 +87,10 @@ _PROTOS = {
     "dt_tree_create": (ctypes.c_int, [_p, _i32, _i32, _i32, _p, _p]),
     "dt_tree_get_info": (ctypes.c_int, [_p, _p]),
     "dt_tree_destroy": (None, [_p]),
-    "dt_tree_launch_info": (ctypes.c_int, [_p, _p, _i64, ctypes.c_int, ctypes.c_int, _p]),
+    "dt_tree_launch_info": (ctypes.c_int, [_p, _p, ctypes.c_int, _i64, ctypes.c_int, ctypes.c_int, _p]),
     "dt_classify": (ctypes.c_int, [_p, _p, _i64, _i64, _p, ctypes.c_int, ctypes.c_int, _p]),
+    "dt_classify_typed": (ctypes.c_int, [_p, _p, ctypes.c_int, _i64, _i64, _p, ctypes.c_int,
+                                         ctypes.c_int, _p]),
     "dt_forest_create": (ctypes.c_int, [_p, _p, _i32, _i32, _i32, _p, _p]),
     "dt_forest_destroy": (None, [_p]),
     "dt_forest_classify": (ctypes.c_int, [_p, _p, _i64, _i64, _p, ctypes.c_int, ctypes.c_int, _p]),
@@ -169,11 +172,20 @@ def _stream_handle(stream) -> Optional[int]:
     return stream.cuda_stream
 
 
-def _features_arg(x, n_features: int):
+def _x_type(x) -> int:
+    """dt_dtype of a record tensor: float32, float16, bfloat16 or uint8."""
+    import torch
+    types = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2, torch.uint8: 3}
+    if x.dtype not in types:
+        raise TypeError("records must be float32, float16, bfloat16 or uint8, not %s" % x.dtype)
+    return types[x.dtype]
+
+
+def _features_arg(x, n_features: int, typed: bool = False):
     import torch
     if not isinstance(x, torch.Tensor) or x.device.type != "cuda":
         raise TypeError("features must be a CUDA (HIP) torch tensor")
-    if x.dtype != torch.float32 or x.dim() != 2:
+    if x.dim() != 2 or (not typed and x.dtype != torch.float32):
         raise TypeError("features must be a 2-D float32 tensor")
     if x.shape[1] < n_features:
         raise ValueError("features has %d columns, tree needs %d" % (x.shape[1], n_features))
@@ -214,20 +226,21 @@ class Tree:
 
     def launch_info(self, x, algo: str = "data", out_kind: str = "class_u8") -> dict:
         """Launch shape classify() uses for ``x`` (diagnostic)."""
-        ptr, _, ld = _features_arg(x, self.n_features)
+        ptr, _, ld = _features_arg(x, self.n_features, typed=True)
         info = LaunchInfo()
-        _check(_lib.dt_tree_launch_info(self._h, ptr, ld, OUT_KINDS[out_kind], ALGOS[algo],
-                                        ctypes.byref(info)), "dt_tree_launch_info")
+        _check(_lib.dt_tree_launch_info(self._h, ptr, _x_type(x), ld, OUT_KINDS[out_kind],
+                                        ALGOS[algo], ctypes.byref(info)), "dt_tree_launch_info")
         return info.as_dict()
 
     def classify(self, x, algo: str = "data", out_kind: str = "class_u8", out=None, stream=None):
-        """Labels (or leaf indices) of the rows of ``x``; asynchronous on ``stream``
-        (default: torch's current stream)."""
-        ptr, n, ld = _features_arg(x, self.n_features)
+        """Labels (or leaf indices) of the rows of ``x`` (float32, float16, bfloat16 or uint8
+        records); asynchronous on ``stream`` (default: torch's current stream)."""
+        ptr, n, ld = _features_arg(x, self.n_features, typed=True)
         out = _out_tensor(out, n, out_kind, x.device)
-        _check(_lib.dt_classify(self._h, ptr, n, ld, out.data_ptr() if n else None,
-                                OUT_KINDS[out_kind], ALGOS[algo], _stream_handle(stream)),
-               "dt_classify")
+        _check(_lib.dt_classify_typed(self._h, ptr, _x_type(x), n, ld,
+                                      out.data_ptr() if n else None, OUT_KINDS[out_kind],
+                                      ALGOS[algo], _stream_handle(stream)),
+               "dt_classify_typed")
         return out
 
     def close(self):

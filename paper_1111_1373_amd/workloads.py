@@ -321,6 +321,51 @@ def config(k: int, n_samples: Optional[int] = None) -> TreeWorkload:
     return w
 
 
+# ----------------------------------------------------------------------------------------
+# narrower record types
+
+NARROW_TYPES = ("f16", "bf16", "u8")
+
+
+def _u8_affine(dist: str):
+    """(scale, offset) of the 8-bit quantisation q = clip(floor(scale * x + offset), 0, 255)."""
+    return (256.0, 0.0) if dist == "uniform" else (32.0, 128.0)
+
+
+def narrow_records(x: np.ndarray, x_type: str, dist: str = "uniform") -> np.ndarray:
+    """The fp32 records ``x`` stored as ``x_type``.
+
+    f16: IEEE binary16, round to nearest even (numpy's cast).  bf16: the upper half of the
+    binary32 after round to nearest even, as uint16 bit patterns (inputs must not be NaN).
+    u8: the 8-bit quantisation of ``_u8_affine(dist)`` (ordered discrete values 0..255).
+    """
+    if x_type == "f16":
+        with np.errstate(over="ignore"):     # beyond 65504 rounds to infinity
+            return x.astype(np.float16)
+    if x_type == "bf16":
+        bits = x.view(np.uint32)
+        rounded = bits + np.uint32(0x7FFF) + ((bits >> np.uint32(16)) & np.uint32(1))
+        return (rounded >> np.uint32(16)).astype(np.uint16)
+    if x_type == "u8":
+        a, b = _u8_affine(dist)
+        return np.clip(np.floor(x * np.float32(a) + np.float32(b)), 0, 255).astype(np.uint8)
+    raise ValueError(x_type)
+
+
+def narrow_tree(nodes: np.ndarray, x_type: str, dist: str = "uniform") -> np.ndarray:
+    """A tree for records of ``x_type``: for u8 the thresholds are mapped by the same affine
+    quantisation as the records (so the splits fall on the 8-bit grid's scale); for the
+    floating-point types the tree is unchanged."""
+    if x_type != "u8":
+        return nodes
+    a, b = _u8_affine(dist)
+    out = nodes.copy()
+    internal = out["cls"] < 0
+    out["threshold"][internal] = (out["threshold"][internal] * np.float32(a) +
+                                  np.float32(b)).astype(np.float32)
+    return out
+
+
 CONFIG_DESCRIPTIONS = {
     1: "C1: N=65,536 x F=8 fp32 U[0,1); complete depth-4 tree (15 internal), 4 classes",
     2: "C2: N=262,144 (512x512) x F=16 fp32 U[0,1); complete depth-8 tree (255 internal), 8 classes",

@@ -123,3 +123,29 @@ def boundary_values(nodes, feature):
     # unique by bit pattern (keeps -0.0 and NaN)
     _, idx = np.unique(arr.view(np.uint32), return_index=True)
     return arr[np.sort(idx)]
+
+
+def widen(xn: np.ndarray, x_type: str) -> np.ndarray:
+    """Exact fp32 values of narrow records (the definition the GPU path must match):
+    binary16 and uint8 by numpy's exact casts, bfloat16 bits by placing them in the upper
+    half of a binary32."""
+    if x_type in ("f16", "u8"):
+        return xn.astype(np.float32)
+    if x_type == "bf16":
+        return (xn.astype(np.uint32) << np.uint32(16)).view(np.float32)
+    raise ValueError(x_type)
+
+
+def narrow_specials(x_type: str) -> np.ndarray:
+    """Stored values that stress the widening: signed zeros, subnormals, extremes, infinities
+    and NaN of each type (as the type's storage: float16, uint16 bits or uint8)."""
+    if x_type == "f16":
+        return np.array([0.0, -0.0, 2.0 ** -24, -(2.0 ** -24), 2.0 ** -14, 1023 * 2.0 ** -24,
+                         65504.0, -65504.0, np.inf, -np.inf, np.nan, 1.0, 0.5, 0.099976],
+                        dtype=np.float16)
+    if x_type == "bf16":
+        return np.array([0x0000, 0x8000, 0x0001, 0x8001, 0x007F, 0x0080, 0x7F7F, 0xFF7F,
+                         0x7F80, 0xFF80, 0x7FC0, 0x3F80, 0x3F00, 0x3DCD], dtype=np.uint16)
+    if x_type == "u8":
+        return np.array([0, 1, 2, 127, 128, 254, 255], dtype=np.uint8)
+    raise ValueError(x_type)
