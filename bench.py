@@ -34,16 +34,17 @@ PAPER_CONTEXT = {"speculative_us": 404.466, "data_us": 538.235, "ratio": 404.466
                  "workload": "65,536 records x 19 attributes, 31-node tree"}
 
 
-KERNEL_SOURCES = {"data": "kernels.hip", "speculative": "kernels.hip", "path": "path.hip",
-                  "forest": "forest.hip"}
+KERNEL_SOURCES = {"data": ("kernels.hip", "kernels_impl.hpp"),
+                  "speculative": ("kernels.hip", "kernels_impl.hpp"),
+                  "path": ("path.hip",), "forest": ("forest.hip",)}
 
 
 def kernel_source_hash(algo: str) -> str:
     """Hash of the sources that decide what the kernel of `algo` ("data", "speculative",
     "path" or "forest") does and how it is launched."""
     h = hashlib.sha256()
-    for f in (KERNEL_SOURCES[algo], "kernels.hpp", "device_common.hpp", "dtree.hip",
-              "encode.cpp", "encode.hpp"):
+    for f in KERNEL_SOURCES[algo] + ("kernels.hpp", "device_common.hpp", "dtree.hip",
+                                     "encode.cpp", "encode.hpp"):
         with open(os.path.join(ROOT, "paper_1111_1373_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -66,6 +67,9 @@ def recorded_traffic(workload: str, algo: str):
         return float(kv["hbm_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+W_NARROW = ("f16", "bf16", "u8")
 
 
 def outer_times(dt, model, x_np, want, algo, reps, log):
@@ -123,6 +127,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-narrow", dest="narrow", action="store_false",
                     help="skip the fp16 / bf16 / uint8 record runs")
+    ap.add_argument("--narrow-types", default=",".join(W_NARROW),
+                    help="narrow record types to time (comma-separated)")
+    ap.add_argument("--narrow-algos", default="data,speculative")
     ap.add_argument("--outer-reps", type=int, default=3,
                     help="calls per host-resident scheme timed for the outer time (0: skip)")
     args = ap.parse_args()
@@ -242,7 +249,7 @@ def main() -> int:
     narrow = None
     if not w.is_forest and args.narrow:
         narrow = {}
-        for xt in W.NARROW_TYPES:
+        for xt in args.narrow_types.split(","):
             xn = W.narrow_records(x_np, xt, w.feature_dist)
             nodes_n = W.narrow_tree(w.nodes, xt, w.feature_dist)
             xw = xn.astype(np.float32) if xt != "bf16" else \
@@ -259,7 +266,7 @@ def main() -> int:
                              waves_per_cu=args.waves_per_cu)
             esize = xn.dtype.itemsize
             narrow[xt] = {}
-            for algo in ("data", "speculative"):
+            for algo in args.narrow_algos.split(","):
                 wall, ks, got = timed(tree_n, xd, algo, args.steps, args.warmup)
                 kavg = float(ks.mean())
                 bytes_n = n * (F * esize + 1)
