@@ -78,39 +78,55 @@ def _rows(x: np.ndarray, n_features: int):
     return x, ld
 
 
-def tree_leaves(nodes, x: np.ndarray, n_features: int) -> np.ndarray:
+def _fan_out(call, x: np.ndarray, ld: int, out: np.ndarray, threads: int, name: str):
+    """Run ``call(x_ptr, n, ld, out_ptr)`` over contiguous row chunks on ``threads`` host
+    threads (ctypes releases the GIL during the call).  threads == 1 is one serial call."""
+    n = x.shape[0]
+    bounds = np.linspace(0, n, max(1, min(threads, n)) + 1).astype(np.int64) if n else [0, 0]
+
+    def part(k):
+        lo, hi = int(bounds[k]), int(bounds[k + 1])
+        return call(x.ctypes.data + lo * ld * 4, hi - lo, ld, out.ctypes.data + lo * 4)
+
+    if len(bounds) <= 2:
+        rcs = [part(0)]
+    else:
+        from concurrent.futures import ThreadPoolExecutor
+        with ThreadPoolExecutor(len(bounds) - 1) as pool:
+            rcs = list(pool.map(part, range(len(bounds) - 1)))
+    if any(rc != 0 for rc in rcs):
+        raise OracleError("%s failed: %s" % (name, rcs))
+    return out
+
+
+def tree_leaves(nodes, x: np.ndarray, n_features: int, threads: int = 1) -> np.ndarray:
     """Index of the leaf each row reaches (int32[N])."""
     nd = _nodes(nodes)
     x, ld = _rows(x, n_features)
     out = np.empty(x.shape[0], dtype=np.int32)
-    rc = _load().oracle_tree_leaves(nd.ctypes.data, len(nd), n_features, x.ctypes.data,
-                                    x.shape[0], ld, out.ctypes.data)
-    if rc != 0:
-        raise OracleError("oracle_tree_leaves failed: %d" % rc)
-    return out
+    f = _load().oracle_tree_leaves
+    return _fan_out(lambda xp, n, ld_, op: f(nd.ctypes.data, len(nd), n_features, xp, n, ld_, op),
+                    x, ld, out, threads, "oracle_tree_leaves")
 
 
-def tree_classes(nodes, x: np.ndarray, n_features: int) -> np.ndarray:
+def tree_classes(nodes, x: np.ndarray, n_features: int, threads: int = 1) -> np.ndarray:
     """Class label of each row (int32[N])."""
     nd = _nodes(nodes)
     x, ld = _rows(x, n_features)
     out = np.empty(x.shape[0], dtype=np.int32)
-    rc = _load().oracle_tree_classes(nd.ctypes.data, len(nd), n_features, x.ctypes.data,
-                                     x.shape[0], ld, out.ctypes.data)
-    if rc != 0:
-        raise OracleError("oracle_tree_classes failed: %d" % rc)
-    return out
+    f = _load().oracle_tree_classes
+    return _fan_out(lambda xp, n, ld_, op: f(nd.ctypes.data, len(nd), n_features, xp, n, ld_, op),
+                    x, ld, out, threads, "oracle_tree_classes")
 
 
-def forest_classes(nodes, offsets, x: np.ndarray, n_features: int, n_classes: int) -> np.ndarray:
+def forest_classes(nodes, offsets, x: np.ndarray, n_features: int, n_classes: int,
+                   threads: int = 1) -> np.ndarray:
     """Majority-vote label of each row (int32[N]); ties go to the smallest class id."""
     nd = _nodes(nodes)
     off = np.ascontiguousarray(offsets, dtype=np.int32)
     x, ld = _rows(x, n_features)
     out = np.empty(x.shape[0], dtype=np.int32)
-    rc = _load().oracle_forest_classes(nd.ctypes.data, off.ctypes.data, len(off) - 1,
-                                       n_features, n_classes, x.ctypes.data, x.shape[0], ld,
-                                       out.ctypes.data)
-    if rc != 0:
-        raise OracleError("oracle_forest_classes failed: %d" % rc)
-    return out
+    f = _load().oracle_forest_classes
+    return _fan_out(lambda xp, n, ld_, op: f(nd.ctypes.data, off.ctypes.data, len(off) - 1,
+                                             n_features, n_classes, xp, n, ld_, op),
+                    x, ld, out, threads, "oracle_forest_classes")

@@ -95,6 +95,7 @@ _PROTOS = {
     "dt_forest_destroy": (None, [_p]),
     "dt_forest_classify": (ctypes.c_int, [_p, _p, _i64, _i64, _p, ctypes.c_int, ctypes.c_int, _p]),
     "dt_probe_copy": (ctypes.c_int, [_p, _p, _i64, _p]),
+    "dt_probe_read": (ctypes.c_int, [_p, _i64, _p, _i32, _p]),
     "dt_pipeline_create": (ctypes.c_int, [_i32, _p, _p]),
     "dt_pipeline_destroy": (None, [_p]),
     "dt_classify_host": (ctypes.c_int, [_p, _p, _p, _i64, _i64, _p, ctypes.c_int, ctypes.c_int, _p]),
@@ -375,3 +376,11 @@ class Pipeline:
             self.close()
         except Exception:
             pass
+
+
+def probe_read(src, sink, waves_per_cu: int = 8, stream=None):
+    """Stream-read every byte of the device tensor ``src`` (one kernel); ``sink`` is a
+    device int32 tensor the kernel never writes in practice.  Streaming-read ceiling."""
+    nbytes = src.numel() * src.element_size()
+    _check(_lib.dt_probe_read(src.data_ptr(), nbytes, sink.data_ptr(), int(waves_per_cu),
+                              _stream_handle(stream)), "dt_probe_read")

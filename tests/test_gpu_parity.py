@@ -284,3 +284,20 @@ def test_probe_copy(dt):
     dt.probe_copy(src, dst)
     torch.cuda.synchronize()
     assert torch.equal(src, dst)
+
+
+def test_probe_read(dt):
+    """The streaming-read probe reads any 16-byte multiple and writes nothing."""
+    sink = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+    for n in (4, 4096, (1 << 20) + 12):                 # partial tile, whole tiles, ragged
+        src = torch.arange(n, dtype=torch.int32, device="cuda")
+        for wpc in (1, 8, 32):
+            dt.probe_read(src, sink, wpc)
+    torch.cuda.synchronize()
+    assert int(sink.item()) == 7
+    src = torch.zeros(8, dtype=torch.int32, device="cuda")
+    lib = dt._lib
+    assert lib.dt_probe_read(src.data_ptr(), 20, sink.data_ptr(), 8, None) == dt.DT_ERR_INVALID_ARG
+    assert lib.dt_probe_read(src.data_ptr() + 4, 16, sink.data_ptr(), 8, None) == dt.DT_ERR_INVALID_ARG
+    assert lib.dt_probe_read(src.data_ptr(), 16, sink.data_ptr(), 0, None) == dt.DT_ERR_INVALID_ARG
+    assert lib.dt_probe_read(src.data_ptr(), 0, None, 8, None) == dt.DT_OK
