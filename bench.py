@@ -61,7 +61,8 @@ def recorded_traffic(workload: str, algo: str):
         if "=" in line and not line.lstrip().startswith("#"):
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
-    if kv.get("source_hash") != kernel_source_hash("forest" if workload == "C5" else algo):
+    kernel = "forest" if workload == "C5" else algo.split("_")[0]
+    if kv.get("source_hash") != kernel_source_hash(kernel):
         return None
     try:
         return float(kv["hbm_bytes_per_launch"])
@@ -326,6 +327,7 @@ def main() -> int:
                     "frac_of_peak": bytes_n / kavg / 1e9 / PEAK_HBM_GBPS,
                     "mismatches_vs_oracle": int((got != want_n).sum()),
                     "launch": tree_n.launch_info(xd, algo=algo, out_kind="class_u8"),
+                    "traffic": recorded_traffic(w.name, "%s_%s" % (algo, xt)),
                 }
                 log("narrow", xt, algo, json.dumps(narrow[xt][algo]))
             del xd, tree_n
