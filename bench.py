@@ -111,6 +111,91 @@ def outer_times(dt, model, x_np, want, algo, reps, log):
             "note": "PCIe-inclusive; records start and labels end in host memory"}
 
 
+def geometry_sweep(args) -> int:
+    """Tree geometry x record order (Section 6's further work) at 2048 x 2048 records of
+    32 fp32 features: kernel times of every decomposition, checked against the oracle."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_1111_1373_amd import dtree as dt
+    from paper_1111_1373_amd import workloads as W
+
+    def log(*a):
+        print("[sweep]", *a, file=sys.stderr, flush=True)
+
+    F, C, H = 32, 8, 2048
+    n = H * H
+    stream = torch.cuda.current_stream()
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    out = torch.empty(n, dtype=torch.uint8, device="cuda")
+    base = {}
+
+    def rows_for(order, root_feature):
+        if order == "sorted":       # the i.i.d. records, sorted by the root's attribute
+            xi = rows_for("iid", 0)
+            return np.ascontiguousarray(xi[np.argsort(xi[:, root_feature], kind="stable")])
+        if order not in base:
+            base[order] = W.sweep_rows(order, H, H, F)
+        return base[order]
+
+    results = []
+    algos = ["data", "speculative", "path"] if args.algos == "auto" else args.algos.split(",")
+    geometries = W.GEOMETRIES if args.sweep_geometries == "all" else args.sweep_geometries.split(",")
+    orders = W.ORDERS if args.sweep_orders == "all" else args.sweep_orders.split(",")
+    for geometry in geometries:
+        nodes = W.sweep_tree(geometry, F, C)
+        depth = np.zeros(len(nodes), dtype=np.int64)
+        for i in range(len(nodes)):
+            if nodes["cls"][i] < 0:
+                depth[nodes["left"][i]] = depth[nodes["left"][i] + 1] = depth[i] + 1
+        tree = dt.Tree(nodes, F, C, data_window_depth=args.data_window_depth,
+                       spec_window_depth=args.spec_window_depth, waves_per_cu=args.waves_per_cu)
+        info = tree.info
+        for order in orders:
+            x_np = rows_for(order, int(nodes["feature"][0]))
+            leaves = oracle.tree_leaves(nodes, x_np, F, threads=threads)
+            want = nodes["cls"][leaves].astype(np.int32)
+            path = depth[leaves]
+            x = torch.from_numpy(x_np).cuda()
+            r = {"geometry": geometry, "order": order, "tree_depth": int(depth.max()),
+                 "decision_nodes": int((nodes["cls"] < 0).sum()),
+                 "mean_path": float(path.mean()), "max_path": int(path.max()),
+                 "same_leaf_as_previous_record": float((leaves[1:] == leaves[:-1]).mean()),
+                 "data_window_depth": info["data_window_depth"], "data_levels": info["data_levels"],
+                 "spec_window_depth": info["spec_window_depth"], "spec_levels": info["spec_levels"]}
+            for algo in algos:
+                for _ in range(args.warmup):
+                    tree.classify(x, algo=algo, out=out, stream=stream)
+                ks = []
+                for _ in range(args.steps):
+                    e0 = torch.cuda.Event(enable_timing=True)
+                    e1 = torch.cuda.Event(enable_timing=True)
+                    e0.record(stream)
+                    tree.classify(x, algo=algo, out=out, stream=stream)
+                    e1.record(stream)
+                    ks.append((e0, e1))
+                torch.cuda.synchronize()
+                us = float(np.mean([a.elapsed_time(b) for a, b in ks])) * 1e3
+                r[algo + "_us"] = us
+                r[algo + "_samples_per_s"] = n / (us * 1e-6)
+                r[algo + "_mismatches"] = int((out.cpu().numpy().astype(np.int32) != want).sum())
+            if "speculative_us" in r and "data_us" in r:
+                r["speculative_over_data"] = r["speculative_us"] / r["data_us"]
+            log(json.dumps(r))
+            results.append(r)
+            del x
+    line = {"metric": "samples classified/sec per tree, by tree geometry and record order",
+            "unit": "samples/s", "records": n, "n_features": F, "n_classes": C,
+            "steps": args.steps, "warmup": args.warmup, "dtype": "f32", "data": "synthetic",
+            "results": results,
+            "parity": "bit-exact vs oracle" if all(
+                r[a + "_mismatches"] == 0 for r in results for a in algos)
+            else "MISMATCH"}
+    print(json.dumps(line), flush=True)
+    return 0 if line["parity"] != "MISMATCH" else 1
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -133,7 +218,16 @@ def main() -> int:
     ap.add_argument("--narrow-algos", default="data,speculative")
     ap.add_argument("--outer-reps", type=int, default=3,
                     help="calls per host-resident scheme timed for the outer time (0: skip)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="tree geometry x record order sweep instead of the benchmark line")
+    ap.add_argument("--sweep-geometries", default="all")
+    ap.add_argument("--sweep-orders", default="all")
     args = ap.parse_args()
+    if args.sweep:
+        if args.gpus != 1:
+            print("bench.py measures one GPU", file=sys.stderr)
+            return 2
+        return geometry_sweep(args)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this implementation evaluates one tree on one "

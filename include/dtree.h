@@ -100,7 +100,9 @@ typedef struct dt_forest dt_forest;
  * Evaluation layout options.  Both decompositions cut the tree into blocks ("windows",
  * Section 6) of at most `depth` levels, each embedded in a complete subtree of 2^depth - 1
  * slots.  0 selects the library's choice.
- *   data_window_depth: 1..16.  Default: the depth that makes the tables smallest.
+ *   data_window_depth: 1..16.  Default: the fewest window levels whose tables take at
+ *     most 48 KiB (and leave the LDS room for two fp32 record tiles); ties go to smaller
+ *     tables; if no depth fits, the depth with the smallest tables.
  *   spec_window_depth: 1..6 (a window has at most 63 decision nodes, one 64-lane
  *     wavefront).  2^depth lanes evaluate one record, so 64 / 2^depth records share a
  *     wavefront instruction.  Default: 4 (16 lanes: 15 decision nodes and one idle lane,

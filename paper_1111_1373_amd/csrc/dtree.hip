@@ -121,10 +121,12 @@ dt_status check_options(const dt_tree_options *opt) {
     return DT_OK;
 }
 
-void window_depths(const dt_node *nodes, const dtree::TreeShape &shape,
+void window_depths(const dt_node *nodes, const dtree::TreeShape &shape, int32_t n_features,
                    const dt_tree_options *opt, int *data_d, int *spec_d) {
-    *data_d = (opt && opt->data_window_depth) ? opt->data_window_depth
-                                              : dtree::choose_data_window_depth(nodes, shape);
+    *data_d = (opt && opt->data_window_depth)
+                  ? opt->data_window_depth
+                  : dtree::choose_data_window_depth(nodes, shape,
+                                                    dtree::data_table_budget(n_features));
     *spec_d = (opt && opt->spec_window_depth) ? opt->spec_window_depth
                                               : dtree::choose_spec_window_depth(shape);
 }
@@ -420,7 +422,7 @@ dt_status create_impl(const dt_node *nodes, int32_t n_nodes, int32_t n_features,
     t->row_stride = row_stride_for(n_features);
     if (opt && opt->path_hops) t->path_hops = opt->path_hops;
     int depth[2];
-    window_depths(nodes, shape, opt, &depth[0], &depth[1]);
+    window_depths(nodes, shape, n_features, opt, &depth[0], &depth[1]);
     for (int e = 0; e < 2; ++e) {
         dtree::WindowTables wt;
         dtree::build_windows(nodes, shape, depth[e], &wt);
@@ -786,7 +788,7 @@ dt_status dt_tree_check(const dt_node *nodes, int32_t n_nodes, int32_t n_feature
         if (st != DT_OK) return fail(st, msg);
         if (info) {
             int dd, sd;
-            window_depths(nodes, shape, opt, &dd, &sd);
+            window_depths(nodes, shape, n_features, opt, &dd, &sd);
             fill_info(shape, n_features, n_classes, dd, dtree::count_windows(nodes, shape, dd),
                       dtree::count_levels(shape, dd), sd, dtree::count_windows(nodes, shape, sd),
                       dtree::count_levels(shape, sd), info);

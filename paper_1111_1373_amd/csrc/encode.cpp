@@ -147,18 +147,36 @@ void build_windows(const dt_node *nodes, const TreeShape &shape, int depth, Wind
     }
 }
 
-int choose_data_window_depth(const dt_node *nodes, const TreeShape &shape) {
+int64_t data_table_budget(int32_t n_features) {
+    int rs = 4;
+    while (rs < n_features) rs <<= 1;
+    const int64_t tiles = int64_t(2) * 64 * rs * 4;   // two fp32 record tiles of 64 rows
+    return std::max<int64_t>(0, std::min<int64_t>(kDataTableBudget, kLdsBytes - tiles));
+}
+
+int choose_data_window_depth(const dt_node *nodes, const TreeShape &shape, int64_t max_bytes) {
+    // Every window costs a record D steps and an exit lookup, and the records of a
+    // wavefront wait for the one with the most windows on its path, so fewer levels are
+    // faster as long as the tables stay in the LDS.
     const int max_d = std::min(kMaxWindowDepth, std::max(1, shape.depth));
-    int best = 1;
-    int64_t best_bytes = std::numeric_limits<int64_t>::max();
+    int best = 0, smallest = 1;
+    int32_t best_levels = 0;
+    int64_t best_bytes = 0, smallest_bytes = std::numeric_limits<int64_t>::max();
     for (int d = 1; d <= max_d; ++d) {
         const int64_t bytes = table_bytes(count_windows(nodes, shape, d), d);
-        if (bytes <= best_bytes) {   // ties: deeper windows, fewer levels
+        if (bytes <= smallest_bytes) {   // ties: deeper windows
+            smallest = d;
+            smallest_bytes = bytes;
+        }
+        if (bytes > max_bytes) continue;
+        const int32_t levels = count_levels(shape, d);
+        if (best == 0 || levels < best_levels || (levels == best_levels && bytes < best_bytes)) {
             best = d;
+            best_levels = levels;
             best_bytes = bytes;
         }
     }
-    return best;
+    return best ? best : smallest;
 }
 
 int choose_spec_window_depth(const TreeShape &shape) {

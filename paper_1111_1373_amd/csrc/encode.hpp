@@ -60,8 +60,18 @@ inline int64_t table_bytes(int64_t n_windows, int depth) {
     return n_windows * (int64_t(1) << depth) * 12;
 }
 
-// Library's default window depths (see dt_tree_options in dtree.h).
-int choose_data_window_depth(const dt_node *nodes, const TreeShape &shape);
+// LDS bytes of a gfx950 workgroup, and the most LDS the default data windows may take.
+constexpr int64_t kLdsBytes = 160 * 1024;
+constexpr int64_t kDataTableBudget = 48 * 1024;
+
+// Table bytes the default data window depth may use for records of n_features: at most
+// kDataTableBudget, and room left for two fp32 record tiles.
+int64_t data_table_budget(int32_t n_features);
+
+// Library's default window depths (see dt_tree_options in dtree.h).  Data: the fewest
+// window levels among the depths whose tables fit max_bytes (ties: smaller tables), or the
+// smallest tables if none fits.
+int choose_data_window_depth(const dt_node *nodes, const TreeShape &shape, int64_t max_bytes);
 int choose_spec_window_depth(const TreeShape &shape);
 
 }  // namespace dtree

@@ -256,15 +256,19 @@ def _bfs_nodes(kids, rng, n_features, n_classes, threshold_draw):
 
 
 def paper_shape_tree(rng: np.random.Generator, n_internal: int = 15, depth: int = 11,
-                     n_features: int = 19, n_classes: int = 7) -> np.ndarray:
+                     n_features: int = 19, n_classes: int = 7,
+                     spine_p: Optional[float] = None) -> np.ndarray:
     """Random full binary tree with the shape of the paper's experimental tree
     (Section 4.1: 31 nodes, 16 leaves, depth 11): a root-to-leaf spine of ``depth``
     decision nodes, whose turns are random, plus ``n_internal - depth`` splits of random
-    leaves above the bottom level, so the depth stays ``depth``."""
+    leaves above the bottom level, so the depth stays ``depth``.  With ``spine_p`` the
+    spine's thresholds are drawn so that about that fraction of U[0,1) records reaching a
+    spine node follow the spine (otherwise every threshold is U[0,1))."""
     if n_internal < depth:
         raise ValueError("need at least `depth` decision nodes")
     kids = {0: None}
     dep = {0: 0}
+    spine_right = {}
     nxt = 1
     v = 0
     for _ in range(depth):                       # the spine
@@ -272,7 +276,9 @@ def paper_shape_tree(rng: np.random.Generator, n_internal: int = 15, depth: int 
         for c in (nxt, nxt + 1):
             kids[c] = None
             dep[c] = dep[v] + 1
-        v = nxt + int(rng.integers(0, 2))
+        turn = int(rng.integers(0, 2))
+        spine_right[v] = turn == 1
+        v = nxt + turn
         nxt += 2
     for _ in range(n_internal - depth):          # side splits that keep the depth
         leaves = [u for u, k in kids.items() if k is None and dep[u] < depth - 1]
@@ -282,7 +288,139 @@ def paper_shape_tree(rng: np.random.Generator, n_internal: int = 15, depth: int 
             kids[c] = None
             dep[c] = dep[u] + 1
         nxt += 2
-    return _bfs_nodes(kids, rng, n_features, n_classes, lambda: float(uniform_f32(rng, 1)[0]))
+    if spine_p is None:
+        return _bfs_nodes(kids, rng, n_features, n_classes,
+                          lambda: float(uniform_f32(rng, 1)[0]))
+    order, q, h = [], [0], 0
+    while h < len(q):
+        u = q[h]; h += 1
+        order.append(u)
+        if kids[u] is not None:
+            q += list(kids[u])
+    new_id = {u: i for i, u in enumerate(order)}
+    nodes = np.zeros(len(order), dtype=NODE_DTYPE)
+    for u in order:
+        i = new_id[u]
+        if kids[u] is None:
+            nodes[i] = (0, 0.0, -1, int(rng.integers(0, n_classes)))
+            continue
+        t = float(uniform_f32(rng, 1)[0])
+        if u in spine_right:
+            w = t * (1.0 - spine_p)
+            t = w if spine_right[u] else 1.0 - w
+        nodes[i] = (int(rng.integers(0, n_features)), np.float32(t), new_id[kids[u][0]], -1)
+    return nodes
+
+
+def chain_tree(rng: np.random.Generator, n_internal: int, n_features: int, n_classes: int,
+               p_exit: float = 0.05) -> np.ndarray:
+    """Chain ("caterpillar") tree: every decision node has one leaf child and one decision
+    child, the side of the leaf chosen at random, so the depth is ``n_internal``.  For
+    U[0,1) features each node sends about ``p_exit`` of the records that reach it to its
+    leaf: the threshold is drawn from [0, 2 p_exit) when the chain continues to the right
+    and from [1 - 2 p_exit, 1) when it continues to the left."""
+    kids = {0: None}
+    v, nxt = 0, 1
+    cont_right = {}
+    for _ in range(n_internal):
+        kids[v] = (nxt, nxt + 1)
+        kids[nxt] = None
+        kids[nxt + 1] = None
+        right = bool(rng.integers(0, 2))
+        cont_right[v] = right
+        v = nxt + 1 if right else nxt
+        nxt += 2
+    order, q, h = [], [0], 0
+    while h < len(q):
+        u = q[h]; h += 1
+        order.append(u)
+        if kids[u] is not None:
+            q += list(kids[u])
+    new_id = {u: i for i, u in enumerate(order)}
+    nodes = np.zeros(len(order), dtype=NODE_DTYPE)
+    for u in order:
+        i = new_id[u]
+        if kids[u] is None:
+            nodes[i] = (0, 0.0, -1, int(rng.integers(0, n_classes)))
+        else:
+            w = float(uniform_f32(rng, 1)[0]) * 2 * p_exit
+            t = w if cont_right[u] else 1.0 - w
+            nodes[i] = (int(rng.integers(0, n_features)), np.float32(t), new_id[kids[u][0]], -1)
+    return nodes
+
+
+def coherent_rows(seed: int, height: int, width: int, n_features: int) -> np.ndarray:
+    """Image-like records: the pixels of a ``height`` x ``width`` raster in row-major
+    order, each feature a smooth random field (a sum of four plane waves of 1 to 8 cycles
+    across the image plus 2% pixel noise) mapped through the normal CDF, so that every
+    feature is spread over [0, 1) while neighbouring pixels have close values."""
+    from scipy.special import ndtr
+
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(seed)))
+    yy, xx = np.meshgrid(np.arange(height, dtype=np.float32) / height,
+                         np.arange(width, dtype=np.float32) / width, indexing="ij")
+    out = np.empty((height * width, n_features), dtype=np.float32)
+    for f in range(n_features):
+        g = np.zeros((height, width), dtype=np.float32)
+        for _ in range(4):
+            fx, fy = rng.uniform(1, 8, size=2) * rng.choice([-1, 1], size=2)
+            ph = rng.uniform(0, 2 * np.pi)
+            g += np.cos(np.float32(2 * np.pi) * (np.float32(fx) * xx + np.float32(fy) * yy) +
+                        np.float32(ph))
+        g = g / np.float32(np.sqrt(2.0)) + np.float32(0.02 * 2) * rng.standard_normal(
+            g.shape, dtype=np.float32)
+        out[:, f] = np.minimum(ndtr(g.reshape(-1)).astype(np.float32), np.float32(1 - 2 ** -24))
+    return out
+
+
+GEOMETRIES = ("complete10", "grown", "random1023", "paper15", "chain64")
+ORDERS = ("iid", "coherent", "sorted")
+
+
+def sweep_tree(geometry: str, n_features: int = 32, n_classes: int = 8) -> np.ndarray:
+    """Tree of one geometry of the sweep over tree shapes and record arrangements (the
+    further work of Section 6): a complete depth-10 tree; a breadth-first grown tree
+    (p = 0.85, depth <= 16, <= 1,023 decision nodes); a random full tree of 1,023 decision
+    nodes (random leaf splits); the paper's 15-node, depth-11 shape (about 80% of the
+    records reaching a spine node follow the spine); a 64-deep chain."""
+    seed = SEED_BASE + 100 + GEOMETRIES.index(geometry)
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(seed)))
+    F, C = n_features, n_classes
+    if geometry == "complete10":
+        return complete_tree(rng, 10, F, C)
+    if geometry == "grown":
+        return grown_tree(rng, 0.85, 16, 1023, F, C, "uniform")
+    if geometry == "random1023":
+        return random_full_tree(rng, 1023, F, C)
+    if geometry == "paper15":
+        return paper_shape_tree(rng, 15, 11, F, C, spine_p=0.8)
+    if geometry == "chain64":
+        return chain_tree(rng, 64, F, C)
+    raise ValueError(geometry)
+
+
+def sweep_rows(order: str, height: int = 2048, width: int = 2048, n_features: int = 32,
+               sort_feature: int = 0) -> np.ndarray:
+    """height x width records of one arrangement: i.i.d. U[0,1); image-like coherent
+    fields (``coherent_rows``); or the i.i.d. records sorted by attribute
+    ``sort_feature``."""
+    n = height * width
+    if order == "coherent":
+        return coherent_rows(SEED_BASE + 200, height, width, n_features)
+    x = feature_rows(SEED_BASE + 300, n_features, "uniform", 0, n)
+    if order == "sorted":
+        return np.ascontiguousarray(x[np.argsort(x[:, sort_feature], kind="stable")])
+    if order != "iid":
+        raise ValueError(order)
+    return x
+
+
+def sweep_case(geometry: str, order: str, height: int = 2048, width: int = 2048,
+               n_features: int = 32, n_classes: int = 8):
+    """(nodes, records) of one geometry x order case; "sorted" sorts by the root's
+    attribute."""
+    nodes = sweep_tree(geometry, n_features, n_classes)
+    return nodes, sweep_rows(order, height, width, n_features, int(nodes["feature"][0]))
 
 
 def config(k: int, n_samples: Optional[int] = None) -> TreeWorkload:

@@ -353,3 +353,17 @@ def test_pipeline_argument_errors_on_host():
     assert dt._lib.dt_classify_host(None, None, None, 0, 8, None, 0, 0, None) == dt.DT_ERR_INVALID_ARG
     assert dt._lib.dt_forest_classify_host(None, None, None, 0, 8, None, 0, 0, None) == dt.DT_ERR_INVALID_ARG
     assert dt._lib.dt_pipeline_destroy(None) is None
+
+
+@pytest.mark.parametrize("name,F,want_d,want_levels", [
+    ("C1", 8, 4, 1), ("C2", 16, 8, 1), ("C3", 32, 12, 1), ("C4", 64, 12, 1),
+    ("complete10", 32, 10, 1), ("grown", 32, 12, 1), ("random1023", 32, 4, 7),
+    ("paper15", 32, 11, 1), ("chain64", 32, 8, 8), ("C4", 256, 12, 1)])
+def test_default_data_window_depth(name, F, want_d, want_levels):
+    """The default data windows: fewest levels within 48 KiB of tables (less when wide
+    record tiles need the LDS), ties to smaller tables; with F = 256 no depth fits the
+    32 KiB left, so the smallest tables win (48 KiB at depth 6 and 12, the deeper kept)."""
+    nodes = W.config(int(name[1])).nodes if name.startswith("C") else W.sweep_tree(name)
+    info = dt.tree_check(nodes, F, 64)
+    assert (info["data_window_depth"], info["data_levels"]) == (want_d, want_levels)
+    assert info["data_table_bytes"] <= 48 * 1024 or F == 256

@@ -327,3 +327,51 @@ def test_generator_trees_are_valid(k):
         else:
             depth = {1: 4, 2: 8, 4: 12, 5: 10}[k]
             assert d.max() == depth and n_int == (1 << depth) - 1
+
+
+# ------------------------------------------------------------- sweep generators
+
+def _depths(nodes):
+    d = np.zeros(len(nodes), dtype=np.int64)
+    for i in range(len(nodes)):
+        if nodes["cls"][i] < 0:
+            d[nodes["left"][i]] = d[nodes["left"][i] + 1] = d[i] + 1
+    return d
+
+
+@pytest.mark.parametrize("geometry", W.GEOMETRIES)
+def test_sweep_trees_are_valid_and_shaped(geometry):
+    from paper_1111_1373_amd import dtree as dt
+    nodes = W.sweep_tree(geometry)
+    info = dt.tree_check(nodes, 32, 8)
+    want = {"complete10": (1023, 10), "paper15": (15, 11), "chain64": (64, 64)}
+    if geometry in want:
+        assert (info["n_internal"], info["depth"]) == want[geometry]
+    else:
+        assert info["n_internal"] <= 1023 and info["depth"] <= (16 if geometry == "grown" else 1023)
+    assert info["depth"] == _depths(nodes).max()
+
+
+def test_chain_tree_every_decision_node_has_a_leaf_child():
+    """Each decision node above the deepest one has one leaf and one decision child; the
+    deepest has two leaves."""
+    nodes = W.sweep_tree("chain64")
+    d = _depths(nodes)
+    inner = np.flatnonzero(nodes["cls"] < 0)
+    for i in inner:
+        l = nodes["left"][i]
+        leaf_kids = int(nodes["cls"][l] >= 0) + int(nodes["cls"][l + 1] >= 0)
+        assert leaf_kids == (2 if d[i] == d.max() - 1 else 1)
+
+
+def test_sweep_rows():
+    xc = W.sweep_rows("coherent", 128, 128, 4)
+    xi = W.sweep_rows("iid", 128, 128, 4)
+    xs = W.sweep_rows("sorted", 128, 128, 4, sort_feature=2)
+    for x in (xc, xi, xs):
+        assert x.shape == (128 * 128, 4) and x.dtype == np.float32
+        assert x.min() >= 0 and x.max() < 1
+    assert (np.diff(xs[:, 2]) >= 0).all()
+    np.testing.assert_array_equal(np.sort(xs, axis=0), np.sort(xi, axis=0))
+    # neighbouring pixels of the coherent raster are close, the i.i.d. records are not
+    assert np.abs(np.diff(xc, axis=0)).mean() < 0.1 < 0.3 < np.abs(np.diff(xi, axis=0)).mean()
