@@ -18,6 +18,7 @@
 
 #include <cstdint>
 #include <type_traits>
+#include <utility>
 
 #include "kernels.hpp"
 
@@ -352,31 +353,80 @@ struct Spec {
     __device__ __forceinline__ explicit Spec(int lane)
         : j(lane & (S - 1)), seg_shift(lane & ~(S - 1)) {}
 
-    // One window level for the 64 records.  In round g, the segment starting at lane b
-    // evaluates record b + g, so record r's bits arrive in r's own segment in the round
-    // g == r % S.
+    // Segments of 2, 4 or 16 lanes broadcast a lane's value to its segment with one DPP
+    // move (quad_perm within groups of 4 lanes, row_share within rows of 16); the round
+    // index must then be a compile-time constant.
+    static constexpr bool kDpp = S == 2 || S == 4 || S == 16;
+
+    // Window id of record seg_shift + G, held by lane seg_shift + G, in every lane of the
+    // segment.
+    template <int G>
+    __device__ __forceinline__ int window_of(int w) const {
+        if constexpr (S == 16)
+            return __builtin_amdgcn_update_dpp(0, w, 0x150 + G, 0xF, 0xF, false);   // row_share
+        else if constexpr (S == 4)
+            return __builtin_amdgcn_update_dpp(0, w, G * 0x55, 0xF, 0xF, false);    // quad_perm
+        else   // S == 2: quad_perm [G, G, 2 + G, 2 + G]
+            return __builtin_amdgcn_update_dpp(0, w, G | G << 2 | (2 + G) << 4 | (2 + G) << 6,
+                                               0xF, 0xF, false);
+    }
+
+    // Round g: the segment starting at lane b evaluates record b + g, so record r's bits
+    // arrive in r's own segment in the round g == r % S.
+    __device__ __forceinline__ void round(int g, int wr, Bits &bits, const Slot *slots, bool first,
+                                          const Slot &root, const T *tile) const {
+        const int r = seg_shift + g;
+        const Slot p = first ? root : slots[(wr << D) + j];
+        const float xv = Elem<XT>::widen(tile[r * RS + (p.f ^ swz_el<XT, RS>(r))]);
+        const uint64_t m = __ballot(!(xv < p.t));
+        if (j == g) bits = Bits(m >> seg_shift);
+    }
+
+    // Rounds G0 + G... (a group of 4 or 8: a scheduling barrier after each group keeps the
+    // compiler from holding every round's loads in registers at once).
+    template <int G0, int... G>
+    __device__ __forceinline__ void eval_dpp(std::integer_sequence<int, G...>, Bits &bits,
+                                             const Slot *slots, bool first, const Slot &root,
+                                             int w, const T *tile) const {
+        (round(G0 + G, first ? 0 : window_of<G0 + G>(w), bits, slots, first, root, tile), ...);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+
+    template <int K, int... Q>
+    __device__ __forceinline__ void eval_groups(std::integer_sequence<int, Q...>,
+                                                std::integral_constant<int, K>, Bits &bits,
+                                                const Slot *slots, bool first, const Slot &root,
+                                                int w, const T *tile) const {
+        (eval_dpp<Q * K>(std::make_integer_sequence<int, K>(), bits, slots, first, root, w, tile),
+         ...);
+    }
+
+    // One window level for the 64 records.
     __device__ __forceinline__ Bits eval(const Slot *slots, bool first, const Slot &root, int w,
                                          const T *tile) const {
-        Bits bits = 0;
+        if constexpr (kDpp) {
+            // wide tiles keep a 64-register prefetch buffer live: smaller groups there
+            constexpr int kMaxGroup = RS >= 64 ? 4 : 8;
+            constexpr int kGroup = S < kMaxGroup ? S : kMaxGroup;
+            Bits bits = 0;
+            eval_groups(std::make_integer_sequence<int, S / kGroup>(),
+                        std::integral_constant<int, kGroup>(), bits, slots, first, root, w, tile);
+            return bits;
+        } else {
+            Bits bits = 0;
 #pragma unroll 8
-        for (int g = 0; g < S; ++g) {
-            const int r = seg_shift + g;
-            Slot p;
-            if (first) {
-                p = root;
-            } else {
-                int wr;
-                if constexpr (S == 64)
-                    wr = __builtin_amdgcn_readlane(w, g);
-                else
-                    wr = __shfl(w, r);
-                p = slots[(wr << D) + j];
+            for (int g = 0; g < S; ++g) {
+                int wr = 0;
+                if (!first) {
+                    if constexpr (S == 64)
+                        wr = __builtin_amdgcn_readlane(w, g);
+                    else
+                        wr = __shfl(w, seg_shift + g);
+                }
+                round(g, wr, bits, slots, first, root, tile);
             }
-            const float xv = Elem<XT>::widen(tile[r * RS + (p.f ^ swz_el<XT, RS>(r))]);
-            const uint64_t m = __ballot(!(xv < p.t));
-            if (j == g) bits = Bits(m >> seg_shift);
+            return bits;
         }
-        return bits;
     }
 
     // Exit index reached from the window root (slot 1) by following the bits: p <- 2p + b_p.
