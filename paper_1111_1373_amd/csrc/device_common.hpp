@@ -103,10 +103,22 @@ __device__ __forceinline__ int valid_rows(const Rows &in, int64_t tile) {
     return left < kTileRows ? int(left) : kTileRows;
 }
 
-// Store 4 consecutive words (c % 4 == 0) of row r into the swizzled tile (rows of RSW
-// words; `tile` is the word view of the tile).
-template <int RSW>
+// Tile layouts.  Row-major (the default): row r at word r*RSW, word w at w ^ swz(r).
+// Column-major (fp32 only, used where every lane reads its own record): column c at word
+// c*64, row r at c*64 + r, so lane r always reads bank r, whatever column it asks for.
+enum TileLayout { kRowMajor = 0, kColMajor = 1 };
+
+// Store 4 consecutive words (c % 4 == 0) of row r into the tile (rows of RSW words;
+// `tile` is the word view of the tile).
+template <int RSW, int LAYOUT = kRowMajor>
 __device__ __forceinline__ void put4(float *tile, int r, int c, f32x4 v) {
+    if constexpr (LAYOUT == kColMajor) {
+        tile[(c + 0) * kTileRows + r] = v.x;
+        tile[(c + 1) * kTileRows + r] = v.y;
+        tile[(c + 2) * kTileRows + r] = v.z;
+        tile[(c + 3) * kTileRows + r] = v.w;
+        return;
+    }
     float *row = tile + r * RSW;
     const int s = swz<RSW>(r);
     row[(c + 0) ^ s] = v.x;
@@ -163,13 +175,14 @@ struct VecTile {
         load_clamped(in, tile, lane, (valid_rows(in, tile) * in.n_words) >> 2);
     }
 
+    template <int LAYOUT = kRowMajor>
     __device__ __forceinline__ void store(const Rows &in, float *tile, int lane) const {
         if constexpr (EXACT) {
             constexpr int sh = __builtin_ctz(RSW);
 #pragma unroll
             for (int k = 0; k < kVec; ++k) {
                 const int e = (k * 64 + lane) * 4;
-                put4<RSW>(tile, e >> sh, e & (RSW - 1), v[k]);
+                put4<RSW, LAYOUT>(tile, e >> sh, e & (RSW - 1), v[k]);
             }
         } else {
             const int full = kTileRows * in.n_words / 4;
@@ -179,7 +192,7 @@ struct VecTile {
                 if (q < full) {
                     const uint32_t e = uint32_t(q) * 4u;
                     const int r = int(div_w(e, in));
-                    put4<RSW>(tile, r, int(e) - r * in.n_words, v[k]);
+                    put4<RSW, LAYOUT>(tile, r, int(e) - r * in.n_words, v[k]);
                 }
             }
         }
@@ -188,7 +201,7 @@ struct VecTile {
 
 // Vectorised staging of wide rows (RSW > 64 words) in chunks of 16 vectors per lane,
 // without prefetch (loads clamped to the valid vectors as in VecTile).
-template <int RSW>
+template <int RSW, int LAYOUT = kRowMajor>
 __device__ __forceinline__ void stage_wide(const Rows &in, float *tile, int64_t t, int lane) {
     const int nvec = (valid_rows(in, t) * in.n_words) >> 2;
     const int full = kTileRows * in.n_words / 4;
@@ -208,16 +221,17 @@ __device__ __forceinline__ void stage_wide(const Rows &in, float *tile, int64_t 
             if (q < full) {
                 const uint32_t e = uint32_t(q) * 4u;
                 const int r = int(div_w(e, in));
-                put4<RSW>(tile, r, int(e) - r * in.n_words, v[k]);
+                put4<RSW, LAYOUT>(tile, r, int(e) - r * in.n_words, v[k]);
             }
         }
     }
 }
 
 // General staging: any ld >= F, element-aligned, one element per load.
-template <int XT, int RS>
+template <int XT, int RS, int LAYOUT = kRowMajor>
 __device__ __forceinline__ void stage_scalar(const Rows &in, float *tile_words, int64_t t,
                                              int lane) {
+    static_assert(LAYOUT == kRowMajor || XT == kXF32, "column-major tiles hold fp32 records");
     using T = typename Elem<XT>::T;
     T *tile = reinterpret_cast<T *>(tile_words);
     const T *x = static_cast<const T *>(in.x);
@@ -229,7 +243,10 @@ __device__ __forceinline__ void stage_scalar(const Rows &in, float *tile_words, 
         const int c = int(idx) - r * in.n_features;
         T v = T(0);
         if (r < valid) v = x[(row0 + r) * in.ld + c];
-        tile[r * RS + (c ^ swz_el<XT, RS>(r))] = v;
+        if constexpr (LAYOUT == kColMajor)
+            tile[c * kTileRows + r] = v;
+        else
+            tile[r * RS + (c ^ swz_el<XT, RS>(r))] = v;
     }
 }
 
@@ -241,17 +258,17 @@ template <int XT, int RS>
 constexpr bool has_vec_staging() { return row_words<XT, RS>() >= 4; }
 
 // Stage tile t without register prefetch.
-template <int XT, int RS, int LOAD>
+template <int XT, int RS, int LOAD, int LAYOUT = kRowMajor>
 __device__ __forceinline__ void stage_now(const Rows &in, float *tile, int64_t t, int lane) {
     constexpr int RSW = row_words<XT, RS>();
     if constexpr (LOAD != kLoadScalar && has_vec_staging<XT, RS>() && RSW <= 64) {
         VecTile<RSW, LOAD == kLoadExact> buf;
         buf.load_tail(in, t, lane);
-        buf.store(in, tile, lane);
+        buf.template store<LAYOUT>(in, tile, lane);
     } else if constexpr (LOAD != kLoadScalar && has_vec_staging<XT, RS>()) {
-        stage_wide<RSW>(in, tile, t, lane);
+        stage_wide<RSW, LAYOUT>(in, tile, t, lane);
     } else {
-        stage_scalar<XT, RS>(in, tile, t, lane);
+        stage_scalar<XT, RS, LAYOUT>(in, tile, t, lane);
     }
 }
 
@@ -261,7 +278,9 @@ __device__ __forceinline__ void stage_now(const Rows &in, float *tile, int64_t t
 // window or the result.  One-level lookahead: while node p's feature is read, both children
 // of p are fetched as one 16-byte pair and the comparison selects between them, so each
 // level costs one LDS round trip instead of two dependent ones.
-template <int XT>
+// `row[(f ^ sw) * STRIDE]` is feature f of this lane's record: STRIDE 1 for row-major
+// tiles, kTileRows (and sw = 0) for column-major ones.
+template <int XT, int STRIDE = 1>
 __device__ __forceinline__ int32_t walk_data(const Slot *slots, const int32_t *exits, int D,
                                              int levels, const typename Elem<XT>::T *row, int sw) {
     const int S = 1 << D;
@@ -272,13 +291,13 @@ __device__ __forceinline__ int32_t walk_data(const Slot *slots, const int32_t *e
         int p = 1;
         Slot s = win[1];
         for (int k = 1; k < D; ++k) {
-            const float xv = Elem<XT>::widen(row[s.f ^ sw]);
+            const float xv = Elem<XT>::widen(row[(s.f ^ sw) * STRIDE]);
             const Slot2 kids = *reinterpret_cast<const Slot2 *>(win + 2 * p);
             const bool right = !(xv < s.t);
             p = 2 * p + int(right);
             s = right ? kids.r : kids.l;
         }
-        const float xv = Elem<XT>::widen(row[s.f ^ sw]);
+        const float xv = Elem<XT>::widen(row[(s.f ^ sw) * STRIDE]);
         p = 2 * p + int(!(xv < s.t));
         code = exits[(w << D) + p - S];
         if (code < 0) break;
@@ -290,7 +309,7 @@ __device__ __forceinline__ int32_t walk_data(const Slot *slots, const int32_t *e
 // Data decomposition over K trees at once (forests): the K walks of one record are
 // independent, so interleaving them keeps K LDS dependency chains in flight per lane.
 // Tree i's tables start at base[i]; all trees share the window depth D.
-template <int K>
+template <int K, int STRIDE = 1>
 __device__ __forceinline__ void walk_data_k(const char *const (&base)[K], const int (&slot_bytes)[K],
                                             const int (&levels)[K], int D, const float *row,
                                             int sw, int32_t (&code)[K]) {
@@ -317,7 +336,7 @@ __device__ __forceinline__ void walk_data_k(const char *const (&base)[K], const 
 #pragma unroll
             for (int i = 0; i < K; ++i) {
                 const Slot s = win[i][p[i]];
-                const float xv = row[s.f ^ sw];
+                const float xv = row[(s.f ^ sw) * STRIDE];
                 p[i] = 2 * p[i] + int(!(xv < s.t));
             }
         }
@@ -458,6 +477,22 @@ struct Spec {
     }
 };
 
+// Cooperative copy of n16 16-byte words from global memory into the LDS by the whole
+// workgroup, eight loads in flight per thread (a plain loop would wait for each load's
+// round trip before issuing the next).
+__device__ __forceinline__ void copy_to_lds(int4 *dst, const int4 *src, int n16) {
+    const int step = int(blockDim.x);
+    int i = int(threadIdx.x);
+    for (; i + 7 * step < n16; i += 8 * step) {
+        int4 v[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] = src[i + k * step];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) dst[i + k * step] = v[k];
+    }
+    for (; i < n16; i += step) dst[i] = src[i];
+}
+
 // ---- single-tree kernel scaffolding ------------------------------------------------------
 
 // Window tables: staged into the LDS once per workgroup (TAB_LDS), or read in place from
@@ -468,8 +503,8 @@ __device__ __forceinline__ char *bind_tables(const KArgs &a, int4 *lds, const Sl
     if constexpr (TAB_LDS) {
         const int ns = a.slot_bytes >> 4;
         const int ne = a.exit_bytes >> 4;
-        for (int i = threadIdx.x; i < ns; i += blockDim.x) lds[i] = a.slots[i];
-        for (int i = threadIdx.x; i < ne; i += blockDim.x) lds[ns + i] = a.exits[i];
+        copy_to_lds(lds, a.slots, ns);
+        copy_to_lds(lds + ns, a.exits, ne);
         __syncthreads();
         slots = reinterpret_cast<const Slot *>(lds);
         exits = reinterpret_cast<const int32_t *>(reinterpret_cast<const char *>(lds) + a.slot_bytes);

@@ -58,8 +58,12 @@ __global__ void __launch_bounds__(512) forest_kernel(FArgs a) {
     const int lane = threadIdx.x & 63;
     float *tile = reinterpret_cast<float *>(lds) + wave * (kTileRows * RS);
     int4 *tab = lds + (a.waves * kTileRows * RS) / 4;   // chunk buffer after the tiles
-    const float *row = tile + lane * RS;
-    const int sw = dev::swz<RS>(lane);
+    // The data decomposition reads each lane's own record: column-major tiles make every
+    // such read conflict-free.  The speculative one reads across a record: row-major.
+    constexpr int kLayout = SD == 0 ? dev::kColMajor : dev::kRowMajor;
+    constexpr int kStride = SD == 0 ? kTileRows : 1;
+    const float *row = SD == 0 ? tile + lane : tile + lane * RS;
+    const int sw = SD == 0 ? 0 : dev::swz<RS>(lane);
     const int64_t n_groups = (a.in.n_tiles + a.waves - 1) / a.waves;
 
     // Exit code of this lane's record for the tree whose tables start at `base`.
@@ -67,7 +71,7 @@ __global__ void __launch_bounds__(512) forest_kernel(FArgs a) {
         const Slot *sl = reinterpret_cast<const Slot *>(base);
         const int32_t *ex = reinterpret_cast<const int32_t *>(base + slot_bytes);
         if constexpr (SD == 0) {
-            return dev::walk_data<kXF32>(sl, ex, a.depth, levels, row, sw);
+            return dev::walk_data<kXF32, kStride>(sl, ex, a.depth, levels, row, sw);
         } else {
             const dev::Spec<kXF32, RS, SD> spec(lane);
             const Slot root = sl[spec.j];
@@ -89,9 +93,9 @@ __global__ void __launch_bounds__(512) forest_kernel(FArgs a) {
         dev::wave_sync();
         if (active) {
             if (kPrefetch && t < n_full)
-                buf.store(a.in, tile, lane);
+                buf.template store<kLayout>(a.in, tile, lane);
             else
-                dev::stage_now<kXF32, RS, LOAD>(a.in, tile, t, lane);
+                dev::stage_now<kXF32, RS, LOAD, kLayout>(a.in, tile, t, lane);
         }
         dev::wave_sync();
         if constexpr (kPrefetch) {
@@ -124,7 +128,7 @@ __global__ void __launch_bounds__(512) forest_kernel(FArgs a) {
                                 sb[i] = d.y;
                                 lv[i] = d.z;
                             }
-                            dev::walk_data_k<kIlp>(base, sb, lv, a.depth, row, sw, code);
+                            dev::walk_data_k<kIlp, kStride>(base, sb, lv, a.depth, row, sw, code);
 #pragma unroll
                             for (int i = 0; i < kIlp; ++i) add_vote(votes, ~code[i]);
                         }
@@ -150,7 +154,7 @@ __global__ void __launch_bounds__(512) forest_kernel(FArgs a) {
                                 sb[i] = d.y;
                                 lv[i] = d.z;
                             }
-                            dev::walk_data_k<kIlp>(base, sb, lv, a.depth, row, sw, code);
+                            dev::walk_data_k<kIlp, kStride>(base, sb, lv, a.depth, row, sw, code);
 #pragma unroll
                             for (int i = 0; i < kIlp; ++i) add_vote(votes, ~code[i]);
                         }

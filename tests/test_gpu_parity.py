@@ -301,3 +301,32 @@ def test_probe_read(dt):
     assert lib.dt_probe_read(src.data_ptr() + 4, 16, sink.data_ptr(), 8, None) == dt.DT_ERR_INVALID_ARG
     assert lib.dt_probe_read(src.data_ptr(), 16, sink.data_ptr(), 0, None) == dt.DT_ERR_INVALID_ARG
     assert lib.dt_probe_read(src.data_ptr(), 0, None, 8, None) == dt.DT_OK
+
+
+def test_more_than_2_31_elements(dt):
+    """64-bit indexing: 2.25 x 10^9 feature elements (9 GB) on the device, built by repeating
+    the C4 records; the labels must repeat the oracle's C4 labels."""
+    w = W.config(4)
+    x = w.features()
+    want = oracle.tree_classes(w.nodes, x, w.n_features)
+    xd = _gpu(x)
+    reps, extra = 2, 1_500_001
+    big = torch.cat([xd] * reps + [xd[:extra]])
+    del xd
+    n = big.shape[0]
+    assert n * w.n_features > 2 ** 31
+    print("rows", n, "elements", n * w.n_features, flush=True)
+    t = dt.Tree(w.nodes, w.n_features, w.n_classes)
+    expect = torch.from_numpy(np.concatenate([want] * reps + [want[:extra]]).astype(np.uint8))
+    for algo in ALGOS[:2]:
+        got = t.classify(big, algo=algo).cpu()
+        assert torch.equal(got, expect), algo
+    # strided view of the same memory (scalar loads, 64-bit row offsets)
+    view = big[:, : w.n_features - 1]
+    nodes = w.nodes.copy()
+    inner = nodes["cls"] < 0
+    nodes["feature"][inner] = np.minimum(nodes["feature"][inner], w.n_features - 2)
+    want2 = oracle.tree_classes(nodes, x[-100_000:, : w.n_features - 1], w.n_features - 1)
+    t2 = dt.Tree(nodes, w.n_features - 1, w.n_classes)
+    got2 = t2.classify(view, algo="data").cpu().numpy()
+    np.testing.assert_array_equal(got2[n - extra - 100_000: n - extra].astype(np.int32), want2)
