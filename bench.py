@@ -73,7 +73,7 @@ def recorded_traffic(workload: str, algo: str):
 W_NARROW = ("f16", "bf16", "u8")
 
 
-def outer_times(dt, model, x_np, want, algo, reps, log):
+def outer_times(dt, model, x_np, want, algo, reps, log, narrow_case=None):
     """Outer time (records in host memory, labels back in host memory; Section 4.2) of the
     paper's serial scheme and of the overlapped pipeline, from pageable and page-locked
     buffers, next to the kernel time measured inside the same calls."""
@@ -83,27 +83,32 @@ def outer_times(dt, model, x_np, want, algo, reps, log):
     n, F = x_np.shape
     x_pin = torch.from_numpy(x_np).pin_memory()
     out_pin = torch.empty(n, dtype=torch.uint8).pin_memory()
-    schemes = [("serial_pageable", dict(serial=True), x_np, None),
-               ("pipelined_pageable", dict(), x_np, None),
-               ("pipelined_pinned", dict(), x_pin, out_pin)]
+    schemes = [("serial_pageable", dict(serial=True), x_np, None, model, want),
+               ("pipelined_pageable", dict(), x_np, None, model, want),
+               ("pipelined_pinned", dict(), x_pin, out_pin, model, want)]
+    if narrow_case is not None:    # the same records as uint8, page-locked
+        tree_u8, x_u8, want_u8 = narrow_case
+        schemes.append(("pipelined_pinned_u8", dict(), torch.from_numpy(x_u8).pin_memory(),
+                        out_pin, tree_u8, want_u8))
     res = {}
-    for name, opts, xin, out in schemes:
+    for name, opts, xin, out, mdl, ref in schemes:
         p = dt.Pipeline(F, **opts)
-        p.classify(model, xin, algo=algo, out=out)            # warm-up
+        p.classify(mdl, xin, algo=algo, out=out)              # warm-up
         stats = []
         mism = 0
         for _ in range(reps):
-            got = p.classify(model, xin, algo=algo, out=out)
+            got = p.classify(mdl, xin, algo=algo, out=out)
             stats.append(p.last_stats)
             got = got.numpy() if isinstance(got, torch.Tensor) else got
-            mism += int((got.astype(np.int32) != want).sum())
+            mism += int((got.astype(np.int32) != ref).sum())
         avg = {k: float(np.mean([s[k] for s in stats])) for k in
                ("outer_us", "kernel_us", "h2d_us", "d2h_us")}
         res[name] = dict(avg, chunks=stats[0]["chunks"], calls=reps,
                          outer_min_us=float(min(s["outer_us"] for s in stats)),
                          outer_max_us=float(max(s["outer_us"] for s in stats)),
                          samples_per_s=n / (avg["outer_us"] * 1e-6),
-                         h2d_gbps=n * F * 4 / (avg["h2d_us"] * 1e-6) / 1e9 if avg["h2d_us"] else None,
+                         record_bytes=int(xin.numel() * xin.element_size()) if isinstance(
+                             xin, torch.Tensor) else int(xin.nbytes),
                          mismatches_vs_oracle=mism)
         log("outer", name, json.dumps(res[name]))
         p.close()
@@ -201,7 +206,7 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=4, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--config", type=int, default=4, choices=[0, 1, 2, 3, 4, 5])
     ap.add_argument("--algos", default="auto",
                     help="comma-separated decompositions (data, speculative, path); auto: "
                          "all that the workload supports")
@@ -390,6 +395,7 @@ def main() -> int:
             log("PARITY FAILURE:", algo, mism, "mismatches")
 
     narrow = None
+    narrow_case = None
     if not w.is_forest and args.narrow:
         narrow = {}
         for xt in args.narrow_types.split(","):
@@ -424,11 +430,13 @@ def main() -> int:
                     "traffic": recorded_traffic(w.name, "%s_%s" % (algo, xt)),
                 }
                 log("narrow", xt, algo, json.dumps(narrow[xt][algo]))
-            del xd, tree_n
+            if xt == "u8":
+                narrow_case = (tree_n, xn, want_n)
+            del xd
 
     outer = None
     if args.outer_reps > 0:
-        outer = outer_times(dt, tree, x_np, want, "data", args.outer_reps, log)
+        outer = outer_times(dt, tree, x_np, want, "data", args.outer_reps, log, narrow_case)
 
     # streaming-read ceiling of this device: a plain read of the same feature buffer
     sink = torch.zeros(1, dtype=torch.int32, device="cuda")

@@ -335,6 +335,13 @@ dt_status dt_classify_host(const dt_tree *tree, dt_pipeline *pipeline, const flo
                            int64_t n, int64_t ld, void *h_out, dt_output out_kind,
                            dt_algo algo, dt_pipeline_stats *stats);
 
+/* As dt_classify_host for records of element type x_type (dt_classify_typed): h_x holds
+ * elements of x_type (aligned to the element size), ld counts elements.  Narrow records
+ * cross PCIe in their own width.  Errors: as dt_classify_host and dt_classify_typed. */
+dt_status dt_classify_host_typed(const dt_tree *tree, dt_pipeline *pipeline, const void *h_x,
+                                 dt_dtype x_type, int64_t n, int64_t ld, void *h_out,
+                                 dt_output out_kind, dt_algo algo, dt_pipeline_stats *stats);
+
 /* As dt_classify_host for a forest's majority vote (dt_forest_classify). */
 dt_status dt_forest_classify_host(const dt_forest *forest, dt_pipeline *pipeline,
                                   const float *h_x, int64_t n, int64_t ld, void *h_out,

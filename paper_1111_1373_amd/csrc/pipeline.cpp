@@ -14,6 +14,7 @@
 
 #include <algorithm>
 #include <chrono>
+#include <cstdint>
 #include <cstring>
 #include <functional>
 #include <new>
@@ -42,16 +43,16 @@ enum { kEvIn = 0, kEvKernel, kEvOut, kEvDone, kEvents };
 struct Slot {
     hipStream_t stream = nullptr;
     hipEvent_t ev[kEvents] = {};
-    float *d_x = nullptr;      // chunk_rows x n_features
+    char *d_x = nullptr;       // chunk_rows x n_features x 4 bytes (any record type fits)
     void *d_out = nullptr;     // chunk_rows x 4 bytes
-    float *h_x = nullptr;      // pinned bounce buffer for records
+    char *h_x = nullptr;       // pinned bounce buffer for records
     void *h_out = nullptr;     // pinned bounce buffer for labels
     bool busy = false;         // a chunk is queued and not yet retired
     int64_t row0 = 0, rows = 0;
 };
 
-// Classify `rows` device-resident records (row stride n_features) on `stream`.
-using ClassifyFn = std::function<dt_status(const float *, int64_t, void *, hipStream_t)>;
+// Classify `rows` device-resident records (dense rows of n_features elements) on `stream`.
+using ClassifyFn = std::function<dt_status(const void *, int64_t, void *, hipStream_t)>;
 
 bool is_page_locked(const void *p) {
     if (!p) return false;
@@ -64,19 +65,20 @@ bool is_page_locked(const void *p) {
     return attr.type == hipMemoryTypeHost;
 }
 
-// Copy `rows` records of F floats (source row stride ld) into the dense buffer dst, split
-// over up to `threads` host threads (the calling one included).
-void pack_rows(float *dst, const float *src, int64_t rows, int64_t ld, int32_t F, int threads) {
+// Copy `rows` records of row_bytes bytes (source row stride ld_bytes) into the dense
+// buffer dst, split over up to `threads` host threads (the calling one included).
+void pack_rows(char *dst, const char *src, int64_t rows, int64_t ld_bytes, int64_t row_bytes,
+               int threads) {
     const auto work = [=](int64_t r0, int64_t r1) {
         if (r0 >= r1) return;
-        if (ld == F) {
-            std::memcpy(dst + r0 * F, src + r0 * ld, size_t((r1 - r0) * F) * 4);
+        if (ld_bytes == row_bytes) {
+            std::memcpy(dst + r0 * row_bytes, src + r0 * ld_bytes, size_t((r1 - r0) * row_bytes));
         } else {
             for (int64_t r = r0; r < r1; ++r)
-                std::memcpy(dst + r * F, src + r * ld, size_t(F) * 4);
+                std::memcpy(dst + r * row_bytes, src + r * ld_bytes, size_t(row_bytes));
         }
     };
-    const int64_t bytes = rows * F * 4;
+    const int64_t bytes = rows * row_bytes;
     const int t = int(std::max<int64_t>(1, std::min<int64_t>(threads, bytes / kMinBytesPerThread)));
     const int64_t per = (rows + t - 1) / t;
     std::vector<std::thread> pool;
@@ -203,10 +205,12 @@ void drain(dt_pipeline *p) {
     (void)hipGetLastError();
 }
 
-dt_status run_chunked(dt_pipeline *p, const ClassifyFn &classify, const float *h_x, int64_t n,
-                      int64_t ld, unsigned char *h_out, int esize, dt_pipeline_stats *st) {
+dt_status run_chunked(dt_pipeline *p, const ClassifyFn &classify, const char *h_x, int xsize,
+                      int64_t n, int64_t ld, unsigned char *h_out, int esize,
+                      dt_pipeline_stats *st) {
     const int32_t F = p->n_features;
-    const size_t row_bytes = size_t(F) * 4;
+    const size_t row_bytes = size_t(F) * size_t(xsize);
+    const int64_t ld_bytes = ld * xsize;
     const bool in_pinned = is_page_locked(h_x);
     const bool out_pinned = is_page_locked(h_out);
     st->input_pinned = in_pinned ? 1 : 0;
@@ -223,20 +227,20 @@ dt_status run_chunked(dt_pipeline *p, const ClassifyFn &classify, const float *h
         }
         s.row0 = c * p->chunk_rows;
         s.rows = std::min(p->chunk_rows, n - s.row0);
-        const float *src = h_x + s.row0 * ld;
-        int64_t src_ld = ld;
+        const char *src = h_x + s.row0 * ld_bytes;
+        int64_t src_ld = ld_bytes;
         if (!in_pinned) {   // pack into the slot's pinned buffer (the slot is idle now)
-            pack_rows(s.h_x, src, s.rows, ld, F, p->host_threads);
+            pack_rows(s.h_x, src, s.rows, ld_bytes, int64_t(row_bytes), p->host_threads);
             src = s.h_x;
-            src_ld = F;
+            src_ld = int64_t(row_bytes);
         }
         hipError_t e = hipEventRecord(s.ev[kEvIn], s.stream);
         if (e == hipSuccess) {
-            if (src_ld == F)
+            if (src_ld == int64_t(row_bytes))
                 e = hipMemcpyAsync(s.d_x, src, size_t(s.rows) * row_bytes, hipMemcpyHostToDevice,
                                    s.stream);
             else
-                e = hipMemcpy2DAsync(s.d_x, row_bytes, src, size_t(src_ld) * 4, row_bytes,
+                e = hipMemcpy2DAsync(s.d_x, row_bytes, src, size_t(src_ld), row_bytes,
                                      size_t(s.rows), hipMemcpyHostToDevice, s.stream);
         }
         if (e == hipSuccess) e = hipEventRecord(s.ev[kEvKernel], s.stream);
@@ -273,16 +277,17 @@ dt_status run_chunked(dt_pipeline *p, const ClassifyFn &classify, const float *h
 
 // Section 4.2's scheme: device buffers for all n records allocated and freed per call,
 // blocking copies, the kernel in between.
-dt_status run_serial(dt_pipeline *p, const ClassifyFn &classify, const float *h_x, int64_t n,
-                     int64_t ld, unsigned char *h_out, int esize, dt_pipeline_stats *st) {
+dt_status run_serial(dt_pipeline *p, const ClassifyFn &classify, const char *h_x, int xsize,
+                     int64_t n, int64_t ld, unsigned char *h_out, int esize,
+                     dt_pipeline_stats *st) {
     using clock = std::chrono::steady_clock;
     Slot &s = p->slots[0];
     const int32_t F = p->n_features;
-    const size_t row_bytes = size_t(F) * 4;
+    const size_t row_bytes = size_t(F) * size_t(xsize);
     st->input_pinned = is_page_locked(h_x) ? 1 : 0;
     st->output_pinned = is_page_locked(h_out) ? 1 : 0;
     st->chunks = 1;
-    float *d_x = nullptr;
+    char *d_x = nullptr;
     void *d_out = nullptr;
     if (hipMalloc(reinterpret_cast<void **>(&d_x), size_t(n) * row_bytes) != hipSuccess ||
         hipMalloc(&d_out, size_t(n * esize)) != hipSuccess) {
@@ -293,8 +298,8 @@ dt_status run_serial(dt_pipeline *p, const ClassifyFn &classify, const float *h_
     dt_status rs = DT_OK;
     auto t0 = clock::now();
     hipError_t e = ld == F ? hipMemcpy(d_x, h_x, size_t(n) * row_bytes, hipMemcpyHostToDevice)
-                           : hipMemcpy2D(d_x, row_bytes, h_x, size_t(ld) * 4, row_bytes,
-                                         size_t(n), hipMemcpyHostToDevice);
+                           : hipMemcpy2D(d_x, row_bytes, h_x, size_t(ld) * size_t(xsize),
+                                         row_bytes, size_t(n), hipMemcpyHostToDevice);
     auto t1 = clock::now();
     if (e != hipSuccess) rs = set_hip_error(e, "record copy");
     if (rs == DT_OK) {
@@ -320,9 +325,9 @@ dt_status run_serial(dt_pipeline *p, const ClassifyFn &classify, const float *h_
 }
 
 template <class Obj>
-dt_status classify_host(const Obj *obj, dt_pipeline *p, const float *h_x, int64_t n, int64_t ld,
-                        void *h_out, dt_output out_kind, const ClassifyFn &classify,
-                        dt_pipeline_stats *stats) {
+dt_status classify_host(const Obj *obj, dt_pipeline *p, const void *h_x, dt_dtype x_type,
+                        int64_t n, int64_t ld, void *h_out, dt_output out_kind,
+                        const ClassifyFn &classify, dt_pipeline_stats *stats) {
     using clock = std::chrono::steady_clock;
     const auto t0 = clock::now();
     dt_pipeline_stats st{};
@@ -344,11 +349,15 @@ dt_status classify_host(const Obj *obj, dt_pipeline *p, const float *h_x, int64_
     dt_status rs = classify(nullptr, 0, nullptr, p->slots[0].stream);
     if (rs != DT_OK) return rs;
     if (n > 0 && (!h_x || !h_out)) return set_error(DT_ERR_INVALID_ARG, "null host pointer");
+    const int xsize = x_type == DT_F32 ? 4 : x_type == DT_U8 ? 1 : 2;
+    if ((reinterpret_cast<uintptr_t>(h_x) % uintptr_t(xsize)) != 0)
+        return set_error(DT_ERR_INVALID_ARG, "h_x is not aligned to its element size");
     const int esize = out_kind == DT_OUT_CLASS_U8 ? 1 : 4;
     auto *out = static_cast<unsigned char *>(h_out);
+    const char *x = static_cast<const char *>(h_x);
     if (n > 0)
-        rs = p->serial ? run_serial(p, classify, h_x, n, ld, out, esize, &st)
-                       : run_chunked(p, classify, h_x, n, ld, out, esize, &st);
+        rs = p->serial ? run_serial(p, classify, x, xsize, n, ld, out, esize, &st)
+                       : run_chunked(p, classify, x, xsize, n, ld, out, esize, &st);
     st.outer_us = std::chrono::duration<double, std::micro>(clock::now() - t0).count();
     if (stats) *stats = st;
     return rs;
@@ -382,10 +391,11 @@ dt_status dt_classify_host(const dt_tree *tree, dt_pipeline *pipeline, const flo
     try {
         dtree::clear_error();
         const int32_t F = pipeline ? pipeline->n_features : 0;
-        const ClassifyFn fn = [=](const float *d_x, int64_t rows, void *d_out, hipStream_t s) {
-            return dt_classify(tree, d_x, rows, F, d_out, out_kind, algo, s);
+        const ClassifyFn fn = [=](const void *d_x, int64_t rows, void *d_out, hipStream_t s) {
+            return dt_classify(tree, static_cast<const float *>(d_x), rows, F, d_out, out_kind,
+                               algo, s);
         };
-        return classify_host(tree, pipeline, h_x, n, ld, h_out, out_kind, fn, stats);
+        return classify_host(tree, pipeline, h_x, DT_F32, n, ld, h_out, out_kind, fn, stats);
     } catch (...) {
         if (pipeline) drain(pipeline);
         return set_error(DT_ERR_INVALID_ARG, "unexpected internal error");
@@ -398,10 +408,29 @@ dt_status dt_forest_classify_host(const dt_forest *forest, dt_pipeline *pipeline
     try {
         dtree::clear_error();
         const int32_t F = pipeline ? pipeline->n_features : 0;
-        const ClassifyFn fn = [=](const float *d_x, int64_t rows, void *d_out, hipStream_t s) {
-            return dt_forest_classify(forest, d_x, rows, F, d_out, out_kind, algo, s);
+        const ClassifyFn fn = [=](const void *d_x, int64_t rows, void *d_out, hipStream_t s) {
+            return dt_forest_classify(forest, static_cast<const float *>(d_x), rows, F, d_out,
+                                      out_kind, algo, s);
         };
-        return classify_host(forest, pipeline, h_x, n, ld, h_out, out_kind, fn, stats);
+        return classify_host(forest, pipeline, h_x, DT_F32, n, ld, h_out, out_kind, fn, stats);
+    } catch (...) {
+        if (pipeline) drain(pipeline);
+        return set_error(DT_ERR_INVALID_ARG, "unexpected internal error");
+    }
+}
+
+dt_status dt_classify_host_typed(const dt_tree *tree, dt_pipeline *pipeline, const void *h_x,
+                                 dt_dtype x_type, int64_t n, int64_t ld, void *h_out,
+                                 dt_output out_kind, dt_algo algo, dt_pipeline_stats *stats) {
+    try {
+        dtree::clear_error();
+        if (x_type != DT_F32 && x_type != DT_F16 && x_type != DT_BF16 && x_type != DT_U8)
+            return set_error(DT_ERR_INVALID_ARG, "unknown x_type");
+        const int32_t F = pipeline ? pipeline->n_features : 0;
+        const ClassifyFn fn = [=](const void *d_x, int64_t rows, void *d_out, hipStream_t s) {
+            return dt_classify_typed(tree, d_x, x_type, rows, F, d_out, out_kind, algo, s);
+        };
+        return classify_host(tree, pipeline, h_x, x_type, n, ld, h_out, out_kind, fn, stats);
     } catch (...) {
         if (pipeline) drain(pipeline);
         return set_error(DT_ERR_INVALID_ARG, "unexpected internal error");

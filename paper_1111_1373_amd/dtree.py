@@ -100,6 +100,8 @@ _PROTOS = {
     "dt_pipeline_destroy": (None, [_p]),
     "dt_classify_host": (ctypes.c_int, [_p, _p, _p, _i64, _i64, _p, ctypes.c_int, ctypes.c_int, _p]),
     "dt_forest_classify_host": (ctypes.c_int, [_p, _p, _p, _i64, _i64, _p, ctypes.c_int, ctypes.c_int, _p]),
+    "dt_classify_host_typed": (ctypes.c_int, [_p, _p, _p, ctypes.c_int, _i64, _i64, _p, ctypes.c_int,
+                                              ctypes.c_int, _p]),
 }
 for _name, (_res, _args) in _PROTOS.items():
     _f = getattr(_lib, _name)
@@ -300,22 +302,36 @@ def probe_copy(src, dst, stream=None):
            "dt_probe_copy")
 
 
-def _host_features_arg(x, n_features: int):
-    """(pointer, rows, row stride in floats) of a host float32 matrix (numpy or CPU tensor)."""
+def _host_features_arg(x, n_features: int, x_type=None):
+    """(pointer, rows, row stride in elements, dt_dtype) of a host record matrix (numpy or
+    CPU tensor) of float32, float16, bfloat16 (torch, or numpy uint16 with x_type="bf16")
+    or uint8."""
     import torch
     if isinstance(x, torch.Tensor):
         if x.device.type != "cpu":
             raise TypeError("host features must be a CPU tensor or a numpy array")
-        if x.dtype != torch.float32 or x.dim() != 2:
-            raise TypeError("features must be a 2-D float32 array")
+        if x.dim() != 2:
+            raise TypeError("features must be a 2-D array")
+        xt = _x_type(x)
         rows, cols, st0, st1, ptr = x.shape[0], x.shape[1], x.stride(0), x.stride(1), x.data_ptr()
     else:
-        if not isinstance(x, np.ndarray) or x.dtype != np.float32 or x.ndim != 2:
-            raise TypeError("features must be a 2-D float32 array")
+        if not isinstance(x, np.ndarray) or x.ndim != 2:
+            raise TypeError("features must be a 2-D array")
+        kinds = {np.dtype(np.float32): 0, np.dtype(np.float16): 1, np.dtype(np.uint8): 3}
+        if x.dtype == np.uint16 and x_type == "bf16":
+            xt = 2
+        elif x.dtype in kinds:
+            xt = kinds[x.dtype]
+        else:
+            raise TypeError("host records must be float32, float16, uint8 or (with "
+                            "x_type='bf16') uint16 bfloat16 bits, not %s" % x.dtype)
+        es = x.dtype.itemsize
         rows, cols, ptr = x.shape[0], x.shape[1], x.ctypes.data
-        st0, st1 = x.strides[0] // 4, x.strides[1] // 4
-        if x.strides[0] % 4 or x.strides[1] % 4:
-            raise ValueError("feature strides must be whole floats")
+        if x.strides[0] % es or x.strides[1] % es:
+            raise ValueError("feature strides must be whole elements")
+        st0, st1 = x.strides[0] // es, x.strides[1] // es
+    if x_type is not None and X_TYPES[x_type] != xt:
+        raise TypeError("records are %s, not %s" % ({v: k for k, v in X_TYPES.items()}[xt], x_type))
     if cols < n_features:
         raise ValueError("features has %d columns, tree needs %d" % (cols, n_features))
     if st1 != 1 and cols > 1:
@@ -323,7 +339,7 @@ def _host_features_arg(x, n_features: int):
     ld = st0 if rows > 1 else max(cols, n_features)
     if ld < n_features:
         raise ValueError("row stride smaller than n_features")
-    return ptr, rows, ld
+    return ptr, rows, ld, xt
 
 
 class Pipeline:
@@ -340,12 +356,14 @@ class Pipeline:
                "dt_pipeline_create")
         self.last_stats = None
 
-    def classify(self, model, x, algo: str = "data", out_kind: str = "class_u8", out=None):
+    def classify(self, model, x, algo: str = "data", out_kind: str = "class_u8", out=None,
+                 x_type=None):
         """Labels of the rows of the host matrix ``x`` for a :class:`Tree` or :class:`Forest`,
         in ``out`` (host, allocated if None: numpy for numpy input, else a CPU tensor).
+        Records may be float32, float16, bfloat16 or uint8 (trees; forests read float32).
         Timing of the call is left in ``self.last_stats``."""
         import torch
-        ptr, n, ld = _host_features_arg(x, self.n_features)
+        ptr, n, ld, xt = _host_features_arg(x, self.n_features, x_type)
         np_dtype = np.uint8 if out_kind == "class_u8" else np.int32
         if out is None:
             out = (np.empty(n, dtype=np_dtype) if isinstance(x, np.ndarray)
@@ -360,9 +378,22 @@ class Pipeline:
                 raise ValueError("out must be a contiguous CPU %s tensor of %d elements" % (want, n))
             optr = out.data_ptr()
         st = PipelineStats()
-        fn = _lib.dt_forest_classify_host if isinstance(model, Forest) else _lib.dt_classify_host
-        _check(fn(model._h, self._h, ptr if n else None, n, ld, optr if n else None,
-                  OUT_KINDS[out_kind], ALGOS[algo], ctypes.byref(st)), fn.__name__)
+        if isinstance(model, Forest):
+            if xt != 0:
+                raise TypeError("forests classify float32 records")
+            _check(_lib.dt_forest_classify_host(model._h, self._h, ptr if n else None, n, ld,
+                                                optr if n else None, OUT_KINDS[out_kind],
+                                                ALGOS[algo], ctypes.byref(st)),
+                   "dt_forest_classify_host")
+        elif xt == 0:
+            _check(_lib.dt_classify_host(model._h, self._h, ptr if n else None, n, ld,
+                                         optr if n else None, OUT_KINDS[out_kind], ALGOS[algo],
+                                         ctypes.byref(st)), "dt_classify_host")
+        else:
+            _check(_lib.dt_classify_host_typed(model._h, self._h, ptr if n else None, xt, n, ld,
+                                               optr if n else None, OUT_KINDS[out_kind],
+                                               ALGOS[algo], ctypes.byref(st)),
+                   "dt_classify_host_typed")
         self.last_stats = st.as_dict()
         return out
 

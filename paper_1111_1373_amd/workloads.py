@@ -8,7 +8,10 @@ Node arrays follow the breadth-first encoding of Procedure 1 (Section 3.1): node
 stores ``(feature, threshold, left, cls)``; the right child is ``left + 1``; ``cls = -1``
 marks an internal (decision) node.  Features are 0-based (the paper counts from 1).
 
-The five configurations are the evaluation workloads of this implementation:
+The five configurations C1..C5 are the evaluation workloads of this implementation (C0 is
+the shape of the paper's own experiment, for context):
+
+    C0  N=65,536     F=19  U[0,1)  15 decision nodes, depth 11 (the paper's shape), 7 classes
 
     C1  N=65,536     F=8   U[0,1)  complete depth-4 tree,  4 classes
     C2  N=262,144    F=16  U[0,1)  complete depth-8 tree,  8 classes (512x512 image)
@@ -424,11 +427,17 @@ def sweep_case(geometry: str, order: str, height: int = 2048, width: int = 2048,
 
 
 def config(k: int, n_samples: Optional[int] = None) -> TreeWorkload:
-    """Workload C1..C5 (``k`` in 1..5).  ``n_samples`` may shrink the sample count."""
+    """Workload C0..C5 (``k`` in 0..5).  ``n_samples`` may shrink the sample count.
+
+    C0 is the shape of the paper's own experiment (Section 4.1: 65,536 records of 19
+    attributes, a 31-node tree of depth 11, 7 classes), with synthetic records and tree."""
     seed = SEED_BASE + k
     tree_ss, _ = _streams(seed)
     rng = np.random.Generator(np.random.PCG64(tree_ss))
-    if k == 1:
+    if k == 0:
+        w = TreeWorkload("C0", paper_shape_tree(rng, 15, 11, 19, 7, spine_p=0.8), 19, 7, 65_536,
+                         "uniform", seed)
+    elif k == 1:
         w = TreeWorkload("C1", complete_tree(rng, 4, 8, 4), 8, 4, 65_536, "uniform", seed)
     elif k == 2:
         w = TreeWorkload("C2", complete_tree(rng, 8, 16, 8), 16, 8, 262_144, "uniform", seed)
@@ -453,7 +462,7 @@ def config(k: int, n_samples: Optional[int] = None) -> TreeWorkload:
         w = TreeWorkload("C5", np.concatenate(trees), 32, 8, 4_194_304, "uniform", seed,
                          tree_offsets=offsets)
     else:
-        raise ValueError("config index must be 1..5")
+        raise ValueError("config index must be 0..5")
     if n_samples is not None:
         w.n_samples = int(n_samples)
     return w
@@ -505,6 +514,7 @@ def narrow_tree(nodes: np.ndarray, x_type: str, dist: str = "uniform") -> np.nda
 
 
 CONFIG_DESCRIPTIONS = {
+    0: "C0: N=65,536 x F=19 fp32 U[0,1); the paper's tree shape (15 internal, depth 11), 7 classes",
     1: "C1: N=65,536 x F=8 fp32 U[0,1); complete depth-4 tree (15 internal), 4 classes",
     2: "C2: N=262,144 (512x512) x F=16 fp32 U[0,1); complete depth-8 tree (255 internal), 8 classes",
     3: "C3: N=2,073,600 (1920x1080) x F=32 fp32 N(0,1); random tree p=0.85, depth<=16, <=1,023 internal, 16 classes",

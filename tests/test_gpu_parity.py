@@ -63,7 +63,7 @@ def test_hand_trees(dt, tree):
 
 # ------------------------------------------------------------------ configurations
 
-@pytest.mark.parametrize("k", [1, 2, 3])
+@pytest.mark.parametrize("k", [0, 1, 2, 3])
 def test_config_full_size(dt, k):
     w = W.config(k)
     x = w.features()

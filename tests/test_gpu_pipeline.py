@@ -154,3 +154,53 @@ def test_host_packing_threads(dt, c3, host_threads):
         got = p.classify(t, xin, algo="speculative")
         np.testing.assert_array_equal(got.astype(np.int32), ref)
         assert p.last_stats["input_pinned"] == 0
+
+
+@pytest.mark.parametrize("x_type", ["f16", "bf16", "u8"])
+@pytest.mark.parametrize("pinned", [False, True])
+def test_narrow_records_from_host(dt, x_type, pinned):
+    """Narrow records cross PCIe in their own width and classify like the widened ones."""
+    from tests import treeutil as TU
+    w = W.config(3, n_samples=150_001)
+    xn = W.narrow_records(w.features(), x_type, w.feature_dist)
+    nodes = W.narrow_tree(w.nodes, x_type, w.feature_dist)
+    want = oracle.tree_classes(nodes, TU.widen(xn, x_type), w.n_features)
+    t = dt.Tree(nodes, w.n_features, w.n_classes)
+    for serial in (False, True):
+        p = dt.Pipeline(w.n_features, chunk_rows=0 if serial else 20_000, serial=serial)
+        if pinned:
+            xin = torch.from_numpy(xn.view(np.int16) if x_type == "bf16" else xn)
+            if x_type == "bf16":
+                xin = xin.view(torch.bfloat16)
+            xin = xin.pin_memory()
+            got = p.classify(t, xin, algo="speculative").numpy()
+        else:
+            got = p.classify(t, xn, algo="data", x_type=x_type if x_type == "bf16" else None)
+        np.testing.assert_array_equal(got.astype(np.int32), want)
+        assert p.last_stats["input_pinned"] == int(pinned)
+    # strided rows
+    wide = np.zeros((xn.shape[0], w.n_features + 3), dtype=xn.dtype)
+    wide[:, : w.n_features] = xn
+    p = dt.Pipeline(w.n_features, chunk_rows=7_000)
+    got = p.classify(t, wide[:, : w.n_features], x_type=x_type if x_type == "bf16" else None)
+    np.testing.assert_array_equal(got.astype(np.int32), want)
+
+
+def test_narrow_host_errors(dt):
+    w = W.config(2, n_samples=100)
+    t = dt.Tree(w.nodes, w.n_features, w.n_classes)
+    f = dt.Forest(W.config(5, n_samples=1).nodes, W.config(5).tree_offsets, 32, 8)
+    p = dt.Pipeline(w.n_features)
+    xh = W.narrow_records(w.features(), "f16")
+    with pytest.raises(TypeError):
+        p.classify(t, xh.view(np.uint16))                   # uint16 needs x_type="bf16"
+    with pytest.raises(TypeError):
+        dt.Pipeline(32).classify(f, np.zeros((4, 32), dtype=np.float16))
+    out = np.zeros(100, dtype=np.uint8)
+    lib = dt._lib
+    assert lib.dt_classify_host_typed(t._h, p._h, xh.ctypes.data, 9, 100, w.n_features,
+                                      out.ctypes.data, 0, 0, None) == dt.DT_ERR_INVALID_ARG
+    assert lib.dt_classify_host_typed(t._h, p._h, xh.ctypes.data + 1, 1, 99, w.n_features,
+                                      out.ctypes.data, 0, 0, None) == dt.DT_ERR_INVALID_ARG
+    assert lib.dt_classify_host_typed(t._h, p._h, xh.ctypes.data, 1, 100, w.n_features,
+                                      out.ctypes.data, 0, 2, None) == dt.DT_ERR_UNSUPPORTED

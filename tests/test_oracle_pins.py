@@ -308,7 +308,7 @@ def test_generator_slices_are_consistent():
     np.testing.assert_array_equal(w.features(1000, start=65000), full[65000:66000])
 
 
-@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("k", [0, 1, 2, 3, 4, 5])
 def test_generator_trees_are_valid(k):
     w = W.config(k, n_samples=16)
     offs = w.tree_offsets if w.is_forest else np.array([0, len(w.nodes)])
@@ -324,6 +324,8 @@ def test_generator_trees_are_valid(k):
         d = TU.depths(nodes)
         if k == 3:
             assert 512 <= n_int <= 1023 and d.max() <= 16
+        elif k == 0:
+            assert d.max() == 11 and n_int == 15          # the paper's 31-node tree shape
         else:
             depth = {1: 4, 2: 8, 4: 12, 5: 10}[k]
             assert d.max() == depth and n_int == (1 << depth) - 1
