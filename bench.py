@@ -262,7 +262,7 @@ def main() -> int:
                          spec_window_depth=args.spec_window_depth,
                          waves_per_cu=args.waves_per_cu)
         info = {"n_trees": len(w.tree_offsets) - 1, "data_window_depth": "auto",
-                "spec_window_depth": 4}
+                "spec_window_depth": args.spec_window_depth or 2}
         oracle_call = lambda: oracle.forest_classes(w.nodes, w.tree_offsets, x_np, F, w.n_classes)
     else:
         tree = dt.Tree(w.nodes, w.n_features, w.n_classes,

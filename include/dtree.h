@@ -105,9 +105,9 @@ typedef struct dt_forest dt_forest;
  *     tables; if no depth fits, the depth with the smallest tables.
  *   spec_window_depth: 1..6 (a window has at most 63 decision nodes, one 64-lane
  *     wavefront).  2^depth lanes evaluate one record, so 64 / 2^depth records share a
- *     wavefront instruction.  Default: 4 (16 lanes: 15 decision nodes and one idle lane,
- *     the half-warp record groups of the paper's experiment, Section 4.2), or the tree
- *     depth if smaller.
+ *     wavefront instruction.  Default: 2 (4 lanes per record, measured fastest), or the
+ *     tree depth if smaller; 4 gives the paper's record groups of 16 lanes (15 decision
+ *     nodes and one idle lane, Section 4.2).  Forests accept 2 (default) or 4.
  */
 typedef struct {
     int32_t data_window_depth;

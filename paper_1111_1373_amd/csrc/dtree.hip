@@ -469,7 +469,8 @@ void destroy_impl(dt_tree *t) {
 
 // ---- forests ---------------------------------------------------------------------------
 
-constexpr int kForestSpecDepth = 4;
+// Speculative forests use windows of depth 2 (default) or 4.
+constexpr int kForestSpecDepth = 2;
 
 int vote_words_for(int32_t n_classes) {
     if (n_classes <= 8) return 2;
@@ -650,8 +651,9 @@ dt_status forest_create_impl(const dt_node *nodes, const int32_t *offsets, int32
         return fail(DT_ERR_INVALID_ARG, "n_features and n_classes must be >= 1");
     dt_status st = check_options(opt);
     if (st != DT_OK) return st;
-    if (opt && opt->spec_window_depth != 0 && opt->spec_window_depth != kForestSpecDepth)
-        return fail(DT_ERR_UNSUPPORTED, "forests use speculative windows of depth 4");
+    if (opt && opt->spec_window_depth != 0 && opt->spec_window_depth != 2 &&
+        opt->spec_window_depth != 4)
+        return fail(DT_ERR_UNSUPPORTED, "forests use speculative windows of depth 2 or 4");
     if (n_trees > dtree::kMaxForestTrees)
         return fail(DT_ERR_UNSUPPORTED, "forests are limited to 255 trees");
     if (n_classes > dtree::kMaxForestClasses)
@@ -690,7 +692,8 @@ dt_status forest_create_impl(const dt_node *nodes, const int32_t *offsets, int32
             if (best < 0 || total <= best) { best = total; data_d = d; }
         }
     }
-    const int depth[2] = {data_d, kForestSpecDepth};
+    const int spec_d = opt && opt->spec_window_depth ? opt->spec_window_depth : kForestSpecDepth;
+    const int depth[2] = {data_d, spec_d};
     for (int algo = 0; algo < 2; ++algo) {
         std::vector<unsigned char> bytes;
         encode_forest(nodes, offsets, n_trees, shapes, depth[algo], &bytes, &f->enc[algo]);

@@ -180,7 +180,7 @@ int choose_data_window_depth(const dt_node *nodes, const TreeShape &shape, int64
 }
 
 int choose_spec_window_depth(const TreeShape &shape) {
-    return std::max(1, std::min(4, shape.depth));
+    return std::max(1, std::min(kDefaultSpecWindowDepth, shape.depth));
 }
 
 }  // namespace dtree

@@ -24,6 +24,9 @@ namespace dtree {
 constexpr int kMaxNodes = 1 << 24;
 constexpr int kMaxWindowDepth = 16;
 constexpr int kMaxSpecWindowDepth = 6;
+// Default speculative window depth: 4-lane record groups measured fastest on MI355X (the
+// paper's 16-lane groups are depth 4).
+constexpr int kDefaultSpecWindowDepth = 2;
 
 // Parsed, validated tree.
 struct TreeShape {

@@ -176,6 +176,8 @@ template <int RS, int LOAD, bool TAB_LDS, int NV>
 const void *for_votes(int algo, int depth) {
     if (algo == kAlgoData)
         return reinterpret_cast<const void *>(&forest_kernel<RS, LOAD, TAB_LDS, NV, 0>);
+    if (depth == 2)
+        return reinterpret_cast<const void *>(&forest_kernel<RS, LOAD, TAB_LDS, NV, 2>);
     if (depth == 4)
         return reinterpret_cast<const void *>(&forest_kernel<RS, LOAD, TAB_LDS, NV, 4>);
     return nullptr;

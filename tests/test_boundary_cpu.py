@@ -304,12 +304,12 @@ def test_default_depths_and_info():
     w = W.config(4, n_samples=1)
     info = dt.tree_check(w.nodes, w.n_features, w.n_classes)
     assert info["depth"] == 12 and info["n_internal"] == 4095
-    assert info["spec_window_depth"] == 4 and info["spec_levels"] == 3
+    assert info["spec_window_depth"] == 2 and info["spec_levels"] == 6
     assert info["data_window_depth"] == 12 and info["data_windows"] == 1
     assert info["data_table_bytes"] == 4096 * 12
     w1 = W.config(1, n_samples=1)
     i1 = dt.tree_check(w1.nodes, w1.n_features, w1.n_classes)
-    assert i1["spec_window_depth"] == 4 and i1["spec_windows"] == 1 and i1["spec_levels"] == 1
+    assert i1["spec_window_depth"] == 2 and i1["spec_windows"] == 5 and i1["spec_levels"] == 2
 
 
 # ----------------------------------------------------------------------- forests (host checks)
