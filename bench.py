@@ -236,7 +236,7 @@ def main() -> int:
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this implementation evaluates one tree on one "
-              "device (sharding across GPUs is described in DESIGN.md, not run).",
+              "device; sharding across GPUs is not run.",
               file=sys.stderr)
         return 2
 
