@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define DT_ABI_VERSION 3
+#define DT_ABI_VERSION 4
 
 typedef enum {
     DT_OK = 0,
@@ -175,6 +175,23 @@ dt_status dt_encode_windows(const dt_node *nodes, int32_t n_nodes, int32_t n_fea
                             int32_t n_classes, int32_t window_depth, int32_t capacity_windows,
                             int32_t *features, float *thresholds, int32_t *exit_class,
                             int32_t *exit_leaf, int32_t *n_windows, int32_t *levels);
+
+/*
+ * Keys the kernels for narrow records compare against (host only).  Records of type fp16,
+ * bf16 or uint8 are compared in their own type: each threshold t is moved onto the type's
+ * grid, rounded up, as key[i]:
+ *   DT_F16, DT_BF16  the bits of the smallest non-NaN value of the type that is >= t
+ *                    (-0 for t = 0; +inf above the largest finite value); a NaN threshold
+ *                    gives a quiet NaN (0x7E00, 0x7FC0).
+ *   DT_U8            the smallest integer k in 0..256 with k >= t; 0 for t <= 0 or NaN.
+ * No value of the type lies in [t, key), so for every record value x the kernels'
+ * test "x < key" (fp16/bf16) or "x < key" on integers (uint8) equals the decision x < t of
+ * Procedure 1 on the widened value, and a NaN t sends every record right either way.
+ *   thresholds  host array of n floats; keys: host array of n uint16 (caller-owned)
+ * Errors: DT_ERR_INVALID_ARG for n < 0, null buffers with n > 0, or a type other than
+ * DT_F16, DT_BF16, DT_U8.
+ */
+dt_status dt_threshold_keys(const float *thresholds, int64_t n, dt_dtype type, uint16_t *keys);
 
 /*
  * Validate a tree, encode it for both decompositions and copy the encodings to the

@@ -73,6 +73,45 @@ template <> struct Elem<kXU8> {
     static __device__ __forceinline__ float widen(uint8_t b) { return float(b); }
 };
 
+// Window-table slots as the kernels for record type XT read them.
+//   fp32 records: Slot {float t; int32 f} (8 bytes), decision !(x < t).
+//   Narrow records: one 32-bit word, the feature index in the high half and in the low
+//   half a key on the record type's grid (built on the host, see encode.hpp): for fp16 and
+//   bf16 the threshold rounded up to the nearest value of the type, for uint8 its integer
+//   ceiling clamped to 0..256.  No value of the type lies strictly between t and the key,
+//   so !(x < key) on the stored element is the decision !(x < t) on its widened value.
+template <int XT> struct Node;
+template <> struct Node<kXF32> {
+    using S = Slot;
+    using Pair = Slot2;
+    static __device__ __forceinline__ int feature(const Slot &s) { return s.f; }
+    static __device__ __forceinline__ bool right(float x, const Slot &s) { return !(x < s.t); }
+};
+template <> struct Node<kXF16> {
+    using S = uint32_t;
+    struct alignas(8) Pair { uint32_t l, r; };
+    static __device__ __forceinline__ int feature(uint32_t s) { return int(s >> 16); }
+    static __device__ __forceinline__ bool right(uint16_t x, uint32_t s) {
+        return !(Elem<kXF16>::widen(x) < Elem<kXF16>::widen(uint16_t(s)));
+    }
+};
+template <> struct Node<kXBF16> {
+    using S = uint32_t;
+    struct alignas(8) Pair { uint32_t l, r; };
+    static __device__ __forceinline__ int feature(uint32_t s) { return int(s >> 16); }
+    static __device__ __forceinline__ bool right(uint16_t x, uint32_t s) {
+        return !(Elem<kXBF16>::widen(x) < Elem<kXBF16>::widen(uint16_t(s)));
+    }
+};
+template <> struct Node<kXU8> {
+    using S = uint32_t;
+    struct alignas(8) Pair { uint32_t l, r; };
+    static __device__ __forceinline__ int feature(uint32_t s) { return int(s >> 16); }
+    static __device__ __forceinline__ bool right(uint8_t x, uint32_t s) {
+        return uint32_t(x) >= (s & 0xFFFFu);
+    }
+};
+
 // Element-level position swizzle for rows of RS elements of type XT: the word swizzle,
 // scaled to elements (the position of an element within its word is unchanged).
 template <int XT, int RS>
@@ -281,24 +320,28 @@ __device__ __forceinline__ void stage_now(const Rows &in, float *tile, int64_t t
 // `row[(f ^ sw) * STRIDE]` is feature f of this lane's record: STRIDE 1 for row-major
 // tiles, kTileRows (and sw = 0) for column-major ones.
 template <int XT, int STRIDE = 1>
-__device__ __forceinline__ int32_t walk_data(const Slot *slots, const int32_t *exits, int D,
-                                             int levels, const typename Elem<XT>::T *row, int sw) {
+__device__ __forceinline__ int32_t walk_data(const typename Node<XT>::S *slots,
+                                             const int32_t *exits, int D, int levels,
+                                             const typename Elem<XT>::T *row, int sw) {
+    using N = Node<XT>;
+    using NS = typename N::S;
+    using Pair = typename N::Pair;
     const int S = 1 << D;
     int w = 0;
     int32_t code = -1;
     for (int level = 0; level < levels; ++level) {
-        const Slot *win = slots + (w << D);
+        const NS *win = slots + (w << D);
         int p = 1;
-        Slot s = win[1];
+        NS s = win[1];
         for (int k = 1; k < D; ++k) {
-            const float xv = Elem<XT>::widen(row[(s.f ^ sw) * STRIDE]);
-            const Slot2 kids = *reinterpret_cast<const Slot2 *>(win + 2 * p);
-            const bool right = !(xv < s.t);
+            const auto xv = row[(N::feature(s) ^ sw) * STRIDE];
+            const Pair kids = *reinterpret_cast<const Pair *>(win + 2 * p);
+            const bool right = N::right(xv, s);
             p = 2 * p + int(right);
             s = right ? kids.r : kids.l;
         }
-        const float xv = Elem<XT>::widen(row[(s.f ^ sw) * STRIDE]);
-        p = 2 * p + int(!(xv < s.t));
+        const auto xv = row[(N::feature(s) ^ sw) * STRIDE];
+        p = 2 * p + int(N::right(xv, s));
         code = exits[(w << D) + p - S];
         if (code < 0) break;
         w = code;
@@ -364,6 +407,8 @@ __device__ __forceinline__ void walk_data_k(const char *const (&base)[K], const 
 template <int XT, int RS, int D>
 struct Spec {
     using T = typename Elem<XT>::T;
+    using N = Node<XT>;
+    using Slot = typename N::S;
     static constexpr int S = 1 << D;
     using Bits = typename std::conditional<(S > 32), uint64_t, uint32_t>::type;
     int j;          // slot evaluated by this lane (slot 0 is padding)
@@ -396,8 +441,8 @@ struct Spec {
                                           const Slot &root, const T *tile) const {
         const int r = seg_shift + g;
         const Slot p = first ? root : slots[(wr << D) + j];
-        const float xv = Elem<XT>::widen(tile[r * RS + (p.f ^ swz_el<XT, RS>(r))]);
-        const uint64_t m = __ballot(!(xv < p.t));
+        const T xv = tile[r * RS + (N::feature(p) ^ swz_el<XT, RS>(r))];
+        const uint64_t m = __ballot(N::right(xv, p));
         if (j == g) bits = Bits(m >> seg_shift);
     }
 
@@ -497,8 +542,8 @@ __device__ __forceinline__ void copy_to_lds(int4 *dst, const int4 *src, int n16)
 
 // Window tables: staged into the LDS once per workgroup (TAB_LDS), or read in place from
 // global memory.  Returns the first LDS byte after the tables (where record tiles start).
-template <bool TAB_LDS>
-__device__ __forceinline__ char *bind_tables(const KArgs &a, int4 *lds, const Slot *&slots,
+template <bool TAB_LDS, class NS>
+__device__ __forceinline__ char *bind_tables(const KArgs &a, int4 *lds, const NS *&slots,
                                              const int32_t *&exits) {
     if constexpr (TAB_LDS) {
         const int ns = a.slot_bytes >> 4;
@@ -506,11 +551,11 @@ __device__ __forceinline__ char *bind_tables(const KArgs &a, int4 *lds, const Sl
         copy_to_lds(lds, a.slots, ns);
         copy_to_lds(lds + ns, a.exits, ne);
         __syncthreads();
-        slots = reinterpret_cast<const Slot *>(lds);
+        slots = reinterpret_cast<const NS *>(lds);
         exits = reinterpret_cast<const int32_t *>(reinterpret_cast<const char *>(lds) + a.slot_bytes);
         return reinterpret_cast<char *>(lds) + a.slot_bytes + a.exit_bytes;
     } else {
-        slots = reinterpret_cast<const Slot *>(a.slots);
+        slots = reinterpret_cast<const NS *>(a.slots);
         exits = reinterpret_cast<const int32_t *>(a.exits);
         return reinterpret_cast<char *>(lds);
     }

@@ -36,15 +36,18 @@ int row_stride_for(int32_t n_features) {
     return rs;
 }
 
-// Device resources of one window encoding.
+// Device resources of one window encoding: the exits, and the slots once per record
+// type (8-byte fp32 slots; 4-byte words on each narrow type's grid).
 struct Encoding {
     int32_t depth = 0, n_windows = 0, levels = 0;
-    int64_t slot_bytes = 0, exit_bytes = 0;   // padded to 16
-    void *d_mem = nullptr;                    // [slots][exit_class][exit_leaf]
-    const int4 *d_slots = nullptr;
+    int64_t exit_bytes = 0;                        // padded to 16
+    int64_t slot_bytes[dtree::kElemTypes] = {};    // padded to 16
+    // [fp32 slots][exit_class][exit_leaf][fp16 slots][bf16 slots][uint8 slots]
+    void *d_mem = nullptr;
+    const int4 *d_slots[dtree::kElemTypes] = {};
     const int4 *d_exit_class = nullptr;
     const int4 *d_exit_leaf = nullptr;
-    int64_t table_bytes() const { return slot_bytes + exit_bytes; }
+    int64_t table_bytes(int elem_type) const { return slot_bytes[elem_type] + exit_bytes; }
 };
 
 struct DeviceCaps {
@@ -73,17 +76,28 @@ dt_status upload_encoding(const dtree::WindowTables &wt, Encoding *enc) {
     enc->n_windows = wt.n_windows;
     enc->levels = wt.levels;
     const int64_t n_slots = int64_t(wt.n_windows) * wt.slots;
-    enc->slot_bytes = align16(n_slots * 8);
     enc->exit_bytes = align16(n_slots * 4);
-    const int64_t total = enc->slot_bytes + 2 * enc->exit_bytes;
+    int64_t off[dtree::kElemTypes];
+    int64_t total = 0;
+    for (int xt = 0; xt < dtree::kElemTypes; ++xt) {
+        enc->slot_bytes[xt] = align16(n_slots * (xt == dtree::kXF32 ? 8 : 4));
+        off[xt] = total;
+        total += enc->slot_bytes[xt] + (xt == dtree::kXF32 ? 2 * enc->exit_bytes : 0);
+    }
     std::vector<unsigned char> host(size_t(total), 0);
     for (int64_t i = 0; i < n_slots; ++i) {
         std::memcpy(&host[size_t(8 * i)], &wt.threshold[size_t(i)], 4);
         std::memcpy(&host[size_t(8 * i + 4)], &wt.feature[size_t(i)], 4);
     }
-    std::memcpy(&host[size_t(enc->slot_bytes)], wt.exit_class.data(), size_t(n_slots * 4));
-    std::memcpy(&host[size_t(enc->slot_bytes + enc->exit_bytes)], wt.exit_leaf.data(),
+    const int64_t exit_off = enc->slot_bytes[dtree::kXF32];
+    std::memcpy(&host[size_t(exit_off)], wt.exit_class.data(), size_t(n_slots * 4));
+    std::memcpy(&host[size_t(exit_off + enc->exit_bytes)], wt.exit_leaf.data(),
                 size_t(n_slots * 4));
+    std::vector<uint32_t> words;
+    for (int xt = dtree::kXF16; xt < dtree::kElemTypes; ++xt) {
+        dtree::build_narrow_slots(wt, static_cast<dt_dtype>(xt), &words);
+        std::memcpy(&host[size_t(off[xt])], words.data(), size_t(n_slots * 4));
+    }
     hipError_t e = hipMalloc(&enc->d_mem, size_t(total));
     if (e != hipSuccess) {
         enc->d_mem = nullptr;
@@ -92,9 +106,10 @@ dt_status upload_encoding(const dtree::WindowTables &wt, Encoding *enc) {
     e = hipMemcpy(enc->d_mem, host.data(), size_t(total), hipMemcpyHostToDevice);
     if (e != hipSuccess) return hip_fail(e, "hipMemcpy(tables)");
     auto *base = static_cast<unsigned char *>(enc->d_mem);
-    enc->d_slots = reinterpret_cast<const int4 *>(base);
-    enc->d_exit_class = reinterpret_cast<const int4 *>(base + enc->slot_bytes);
-    enc->d_exit_leaf = reinterpret_cast<const int4 *>(base + enc->slot_bytes + enc->exit_bytes);
+    for (int xt = 0; xt < dtree::kElemTypes; ++xt)
+        enc->d_slots[xt] = reinterpret_cast<const int4 *>(base + off[xt]);
+    enc->d_exit_class = reinterpret_cast<const int4 *>(base + exit_off);
+    enc->d_exit_leaf = reinterpret_cast<const int4 *>(base + exit_off + enc->exit_bytes);
     return DT_OK;
 }
 
@@ -382,9 +397,9 @@ dt_status classify_impl(const dt_tree *tree, const void *d_x, dt_dtype x_type, i
 
     dtree::KArgs a{};
     a.in = make_rows(d_x, x_type, n, ld, tree->n_features);
-    a.slots = enc.d_slots;
+    a.slots = enc.d_slots[x_type];
     a.exits = out_kind == DT_OUT_LEAF_I32 ? enc.d_exit_leaf : enc.d_exit_class;
-    a.slot_bytes = int32_t(enc.slot_bytes);
+    a.slot_bytes = int32_t(enc.slot_bytes[x_type]);
     a.exit_bytes = int32_t(enc.exit_bytes);
     a.depth = enc.depth;
     a.levels = enc.levels;
@@ -451,7 +466,7 @@ dt_status create_impl(const dt_node *nodes, int32_t n_nodes, int32_t n_features,
                 if (m != dtree::kLoadScalar && (n_features * dtree::elem_bytes(xt)) % 16 != 0)
                     continue;
                 for (int o = 0; o < 2; ++o)
-                    make_plan(t->caps, algo, xt, t->row_stride, m, enc.depth, enc.table_bytes(),
+                    make_plan(t->caps, algo, xt, t->row_stride, m, enc.depth, enc.table_bytes(xt),
                               o == 0 ? 1 : 4, opt ? opt->waves_per_cu : 0, &pl[o]);
             }
         }
@@ -824,6 +839,16 @@ dt_status dt_tree_check(const dt_node *nodes, int32_t n_nodes, int32_t n_feature
     } catch (...) {
         return fail(DT_ERR_INVALID_ARG, "unexpected internal error");
     }
+}
+
+dt_status dt_threshold_keys(const float *thresholds, int64_t n, dt_dtype type, uint16_t *keys) {
+    g_last_error.clear();
+    if (n < 0) return fail(DT_ERR_INVALID_ARG, "n must be >= 0");
+    if (type != DT_F16 && type != DT_BF16 && type != DT_U8)
+        return fail(DT_ERR_INVALID_ARG, "type must be DT_F16, DT_BF16 or DT_U8");
+    if (n > 0 && (!thresholds || !keys)) return fail(DT_ERR_INVALID_ARG, "null buffer");
+    for (int64_t i = 0; i < n; ++i) keys[i] = uint16_t(dtree::narrow_key(thresholds[i], type));
+    return DT_OK;
 }
 
 dt_status dt_encode_windows(const dt_node *nodes, int32_t n_nodes, int32_t n_features,

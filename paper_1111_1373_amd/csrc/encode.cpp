@@ -3,6 +3,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstring>
 #include <limits>
 
 namespace dtree {
@@ -145,6 +146,65 @@ void build_windows(const dt_node *nodes, const TreeShape &shape, int depth, Wind
         // A root that is itself a leaf (single-node tree) is handled by the loop above:
         // heap node 0 (slot 1) holds the leaf and its always-right exit is the last one.
     }
+}
+
+namespace {
+
+// Exact values of 16-bit float patterns: IEEE binary16 and bfloat16 (the high half of a
+// binary32).
+double f16_value(uint16_t h) {
+    const int e = (h >> 10) & 31;
+    const int m = h & 1023;
+    const double mag = e == 0    ? std::ldexp(double(m), -24)
+                       : e == 31 ? std::numeric_limits<double>::infinity()
+                                 : std::ldexp(double(1024 + m), e - 25);
+    return (h & 0x8000) ? -mag : mag;
+}
+
+double bf16_value(uint16_t h) {
+    const uint32_t u = uint32_t(h) << 16;
+    float f;
+    std::memcpy(&f, &u, 4);
+    return double(f);
+}
+
+// Smallest non-NaN pattern whose value is >= t (t not NaN).  The non-NaN patterns of a
+// sign-magnitude 16-bit format, in increasing value, are indexed 0 .. 2 * inf_bits: index i
+// <= inf_bits is the negative magnitude inf_bits - i (-inf up to -0), index i > inf_bits the
+// positive magnitude i - inf_bits (the smallest subnormal up to +inf).  Binary search.
+template <class Value>
+uint16_t round_up_16(float t, int32_t inf_bits, Value value) {
+    auto bits = [inf_bits](int32_t i) -> uint16_t {
+        return i <= inf_bits ? uint16_t(0x8000 | (inf_bits - i)) : uint16_t(i - inf_bits);
+    };
+    int32_t lo = 0, hi = 2 * inf_bits;   // +inf is >= every t
+    while (lo < hi) {
+        const int32_t mid = lo + (hi - lo) / 2;
+        if (value(bits(mid)) >= double(t))
+            hi = mid;
+        else
+            lo = mid + 1;
+    }
+    return bits(lo);
+}
+
+}  // namespace
+
+uint32_t narrow_key(float t, dt_dtype type) {
+    if (type == DT_U8) {
+        if (std::isnan(t) || t <= 0.0f) return 0u;
+        if (t > 255.0f) return 256u;
+        return uint32_t(std::ceil(t));
+    }
+    if (type == DT_F16) return std::isnan(t) ? 0x7E00u : round_up_16(t, 0x7C00, f16_value);
+    return std::isnan(t) ? 0x7FC0u : round_up_16(t, 0x7F80, bf16_value);
+}
+
+void build_narrow_slots(const WindowTables &wt, dt_dtype type, std::vector<uint32_t> *out) {
+    const size_t n = wt.threshold.size();
+    out->resize(n);
+    for (size_t i = 0; i < n; ++i)
+        (*out)[i] = (uint32_t(wt.feature[i]) << 16) | narrow_key(wt.threshold[i], type);
 }
 
 int64_t data_table_budget(int32_t n_features) {

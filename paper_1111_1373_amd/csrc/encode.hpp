@@ -51,6 +51,15 @@ struct WindowTables {
     std::vector<int32_t> exit_leaf;
 };
 
+// Slot words of the windows for narrow records (fp16, bf16, uint8): feature index << 16 |
+// key, where the key is the threshold moved onto the record type's grid, rounded up: the
+// smallest value of the type (as its bits) not below t, and for uint8 the integer ceiling
+// of t clamped to 0..256.  No representable record value lies in [t, key), so a stored
+// element x satisfies x < key exactly when its widened value is below t.  A NaN threshold
+// sends every record right (key NaN, or 0 for uint8).  One word per slot, slot-major.
+uint32_t narrow_key(float t, dt_dtype type);
+void build_narrow_slots(const WindowTables &wt, dt_dtype type, std::vector<uint32_t> *out);
+
 // Number of windows for window depth D (without building them).
 int64_t count_windows(const dt_node *nodes, const TreeShape &shape, int depth);
 int32_t count_levels(const TreeShape &shape, int depth);

@@ -29,7 +29,7 @@ template <int XT, int RS, int LOAD, bool TAB_LDS>
 __global__ void __launch_bounds__(512) data_kernel(KArgs a) {
     using T = typename dev::Elem<XT>::T;
     extern __shared__ int4 lds[];
-    const Slot *slots;
+    const typename dev::Node<XT>::S *slots;
     const int32_t *exits;
     char *tiles = dev::bind_tables<TAB_LDS>(a, lds, slots, exits);
     const int lane = threadIdx.x & 63;
@@ -46,8 +46,9 @@ __global__ void __launch_bounds__(512) data_kernel(KArgs a) {
 template <int XT, int RS, int LOAD, bool TAB_LDS, int D>
 __global__ void __launch_bounds__(512) spec_kernel(KArgs a) {
     using T = typename dev::Elem<XT>::T;
+    using NS = typename dev::Node<XT>::S;
     extern __shared__ int4 lds[];
-    const Slot *slots;
+    const NS *slots;
     const int32_t *exits;
     char *tiles = dev::bind_tables<TAB_LDS>(a, lds, slots, exits);
     const int lane = threadIdx.x & 63;
@@ -55,7 +56,7 @@ __global__ void __launch_bounds__(512) spec_kernel(KArgs a) {
     uint8_t *obuf;
     dev::wave_buffers<XT, RS>(a, tiles, tile, obuf);
     const dev::Spec<XT, RS, D> spec(lane);
-    const Slot root = slots[spec.j];   // window 0 is shared by every record
+    const NS root = slots[spec.j];   // window 0 is shared by every record
     const T *el = reinterpret_cast<const T *>(tile);
     dev::tile_loop<XT, RS, LOAD>(a, tile, obuf, lane, [&](int64_t) -> int32_t {
         return ~spec.run(slots, exits, a.levels, root, el);

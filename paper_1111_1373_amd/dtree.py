@@ -84,6 +84,7 @@ _PROTOS = {
     "dt_last_error": (ctypes.c_char_p, []),
     "dt_tree_check": (ctypes.c_int, [_p, _i32, _i32, _i32, _p, _p]),
     "dt_encode_windows": (ctypes.c_int, [_p, _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p]),
+    "dt_threshold_keys": (ctypes.c_int, [_p, _i64, ctypes.c_int, _p]),
     "dt_tree_create": (ctypes.c_int, [_p, _i32, _i32, _i32, _p, _p]),
     "dt_tree_get_info": (ctypes.c_int, [_p, _p]),
     "dt_tree_destroy": (None, [_p]),
@@ -166,6 +167,16 @@ def encode_windows(nodes, n_features: int, n_classes: int, window_depth: int) ->
            "dt_encode_windows")
     return dict(feature=feat, threshold=thr, exit_class=ec, exit_leaf=el, levels=lv.value,
                 n_windows=nw.value, depth=window_depth)
+
+
+def threshold_keys(thresholds, x_type: str) -> np.ndarray:
+    """Thresholds moved onto a narrow record type's grid, as the kernels compare them
+    (host only): uint16 bits for "f16" / "bf16", integers 0..256 for "u8"."""
+    t = np.ascontiguousarray(thresholds, dtype=np.float32).ravel()
+    keys = np.empty(t.size, dtype=np.uint16)
+    _check(_lib.dt_threshold_keys(t.ctypes.data, t.size, X_TYPES[x_type], keys.ctypes.data),
+           "dt_threshold_keys")
+    return keys
 
 
 def _stream_handle(stream) -> Optional[int]:

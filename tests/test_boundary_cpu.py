@@ -42,7 +42,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version_and_strings():
-    assert dt.ABI_VERSION == 3
+    assert dt.ABI_VERSION == 4
     for s in range(6):
         assert dt._lib.dt_status_string(s)
     assert dt._lib.dt_status_string(99) == b"unknown status"
@@ -367,3 +367,86 @@ def test_default_data_window_depth(name, F, want_d, want_levels):
     info = dt.tree_check(nodes, F, 64)
     assert (info["data_window_depth"], info["data_levels"]) == (want_d, want_levels)
     assert info["data_table_bytes"] <= 48 * 1024 or F == 256
+
+
+def _grid(x_type):
+    """Every non-NaN value of a narrow type, widened exactly to float64, and its bits."""
+    if x_type == "u8":
+        v = np.arange(256, dtype=np.uint8)
+        return v, v.astype(np.float64)
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    with np.errstate(invalid="ignore"):
+        val = TU.widen(bits.view(np.float16) if x_type == "f16" else bits,
+                       x_type).astype(np.float64)
+    keep = ~np.isnan(val)
+    return bits[keep], val[keep]
+
+
+def _key_thresholds(x_type, seed=3):
+    """Thresholds that stress the rounding: specials, every grid value, its float32
+    neighbours, the midpoints between grid values, and random float32 bit patterns."""
+    _, val = _grid(x_type)
+    g = np.unique(val[np.isfinite(val)]).astype(np.float32)
+    r = np.random.Generator(np.random.PCG64(seed))
+    rand_bits = r.integers(0, 1 << 32, 20_000, dtype=np.uint64).astype(np.uint32)
+    mids = ((g[:-1].astype(np.float64) + g[1:]) / 2).astype(np.float32)
+    specials = np.float32([np.inf, -np.inf, np.nan, 0.0, -0.0, 65504, 65505, 65519, 65520, 1e30,
+                           -1e30, -65504, -65520, 5.96e-8, 2.98e-8, 1e-45, -1e-45, 255, 255.5,
+                           256, -0.5, 0.5, 3.4e38, -3.4e38])
+    return np.concatenate([specials, g, np.nextafter(g, np.float32(np.inf)),
+                           np.nextafter(g, np.float32(-np.inf)), mids,
+                           rand_bits.view(np.float32)])
+
+
+@pytest.mark.parametrize("x_type", ["f16", "bf16", "u8"])
+def test_threshold_keys_are_the_smallest_grid_value_not_below(x_type):
+    t = _key_thresholds(x_type)
+    keys = dt.threshold_keys(t, x_type)
+    _, val = _grid(x_type)
+    srt = np.unique(val)                                  # -0 and +0 are one value
+    with np.errstate(invalid="ignore"):
+        t64 = t.astype(np.float64)
+    nan = np.isnan(t64)
+    if x_type == "u8":
+        want = np.where(nan, 0, np.clip(np.ceil(np.nan_to_num(t64, nan=0.0)), 0, 256))
+        np.testing.assert_array_equal(keys, want.astype(np.uint16))
+        return
+    idx = np.searchsorted(srt, np.where(nan, 0.0, t64), side="left")
+    with np.errstate(invalid="ignore"):
+        got_val = TU.widen(keys.view(np.float16) if x_type == "f16" else keys, x_type).astype(np.float64)
+    assert np.isnan(got_val[nan]).all()
+    np.testing.assert_array_equal(got_val[~nan], srt[idx[~nan]])
+
+
+@pytest.mark.parametrize("x_type", ["f16", "bf16", "u8"])
+def test_threshold_keys_preserve_every_decision(x_type):
+    """Brute force: for every value x of the type, comparing x with the key in the type
+    decides like comparing the widened x with the threshold (NaN records included)."""
+    t = _key_thresholds(x_type)
+    r = np.random.Generator(np.random.PCG64(5))
+    t = np.concatenate([t[:24], r.choice(t, 600, replace=False)])
+    keys = dt.threshold_keys(t, x_type)
+    if x_type == "u8":
+        x = np.arange(256, dtype=np.float64)
+        right_key = x[None, :] >= keys[:, None].astype(np.float64)
+    else:
+        bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+        with np.errstate(invalid="ignore"):
+            x = TU.widen(bits.view(np.float16) if x_type == "f16" else bits,
+                         x_type).astype(np.float64)
+            kv = TU.widen(keys.view(np.float16) if x_type == "f16" else keys,
+                          x_type).astype(np.float64)
+            right_key = ~(x[None, :] < kv[:, None])
+    with np.errstate(invalid="ignore"):
+        right_t = ~(x[None, :] < t.astype(np.float64)[:, None])
+    np.testing.assert_array_equal(right_key, right_t)
+
+
+def test_threshold_keys_errors():
+    lib = dt._lib
+    t = np.zeros(4, dtype=np.float32)
+    k = np.zeros(4, dtype=np.uint16)
+    assert lib.dt_threshold_keys(t.ctypes.data, 4, 0, k.ctypes.data) == dt.DT_ERR_INVALID_ARG
+    assert lib.dt_threshold_keys(t.ctypes.data, -1, 1, k.ctypes.data) == dt.DT_ERR_INVALID_ARG
+    assert lib.dt_threshold_keys(None, 4, 1, k.ctypes.data) == dt.DT_ERR_INVALID_ARG
+    assert lib.dt_threshold_keys(None, 0, 3, None) == dt.DT_OK
