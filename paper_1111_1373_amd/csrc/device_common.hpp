@@ -383,15 +383,19 @@ __device__ __forceinline__ void walk_data_k(const char *const (&base)[K], const 
                 p[i] = 2 * p[i] + int(!(xv < s.t));
             }
         }
+        // Every chain reads its exit, finished or not (a finished chain re-walked its last
+        // window, so the index stays inside that window's exits), and the K reads are
+        // issued together; a chain still running at this level has level < levels[i].
+        int32_t c[K];
+#pragma unroll
+        for (int i = 0; i < K; ++i)
+            c[i] = reinterpret_cast<const int32_t *>(base[i] + slot_bytes[i])[(w[i] << D) + p[i] - S];
         bool all_done = true;
 #pragma unroll
         for (int i = 0; i < K; ++i) {
-            if (code[i] >= 0 && level < levels[i]) {
-                const int32_t *ex = reinterpret_cast<const int32_t *>(base[i] + slot_bytes[i]);
-                const int32_t c = ex[(w[i] << D) + p[i] - S];
-                code[i] = c;
-                if (c >= 0) w[i] = c;
-            }
+            const bool live = code[i] >= 0;
+            w[i] = live && c[i] >= 0 ? c[i] : w[i];
+            code[i] = live ? c[i] : code[i];
             all_done = all_done && code[i] < 0;
         }
         if (__all(all_done)) break;

@@ -525,7 +525,8 @@ void encode_forest(const dt_node *nodes, const int32_t *offsets, int32_t n_trees
 constexpr int kForestWavesPerCu = 16;
 
 // Choose the workgroup shape and the LDS chunks of consecutive trees.
-void chunk_forest(const DeviceCaps &caps, int row_stride, int waves_per_cu, ForestEncoding *enc) {
+void chunk_forest(const DeviceCaps &caps, int algo, int row_stride, int waves_per_cu,
+                  ForestEncoding *enc) {
     const int64_t tile_bytes = dtree::tile_bytes_for(row_stride, dtree::kXF32);
     const int target = waves_per_cu > 0 ? waves_per_cu : kForestWavesPerCu;
     enc->chunks.clear();
@@ -535,7 +536,7 @@ void chunk_forest(const DeviceCaps &caps, int row_stride, int waves_per_cu, Fore
     int64_t best_budget = 0;
     for (int bpc = 1; bpc <= 4; ++bpc) {
         const int64_t per_block = std::min<int64_t>(caps.lds_per_block, caps.lds_per_cu / bpc);
-        for (int w = dtree::kMaxWavesPerBlock; w >= 1; --w) {
+        for (int w = dtree::forest_max_waves(algo, enc->depth, row_stride); w >= 1; --w) {
             const int64_t budget = per_block - w * tile_bytes;
             if (budget < enc->max_tree_bytes) continue;
             const int score = std::min(target, w * bpc);
@@ -621,7 +622,7 @@ dt_status plan_forest(const DeviceCaps &caps, int algo, int row_stride, int load
         }
     }
     int best_waves = 0;
-    for (int w = 1; w <= dtree::kMaxWavesPerBlock; ++w) {
+    for (int w = 1; w <= dtree::forest_max_waves(algo, enc.depth, row_stride); ++w) {
         if (tab_lds && w != enc.waves) continue;     // the chunks were cut for enc.waves
         const int lds = dtree::lds_bytes_for(enc.chunk_lds_bytes,
                                              dtree::tile_bytes_for(row_stride, dtree::kXF32), w);
@@ -713,7 +714,8 @@ dt_status forest_create_impl(const dt_node *nodes, const int32_t *offsets, int32
         std::vector<unsigned char> bytes;
         encode_forest(nodes, offsets, n_trees, shapes, depth[algo], &bytes, &f->enc[algo]);
         if (f->row_stride <= dtree::kMaxRowStride)
-            chunk_forest(f->caps, f->row_stride, opt ? opt->waves_per_cu : 0, &f->enc[algo]);
+            chunk_forest(f->caps, algo, f->row_stride, opt ? opt->waves_per_cu : 0,
+                         &f->enc[algo]);
         else
             f->enc[algo].chunks.push_back(int4{0, n_trees, 0, int(f->enc[algo].table_bytes)});
         if (f->enc[algo].table_bytes > (int64_t(1) << 31) - 1) {

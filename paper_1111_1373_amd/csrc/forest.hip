@@ -18,12 +18,32 @@ namespace {
 
 using dev::Slot;
 
+// The tree and chunk descriptors never change during a launch and are read at wavefront-
+// uniform indices: read them through the constant address space, which makes them scalar
+// loads.  A vector load would share the in-order load counter with the record prefetch, so
+// waiting for a descriptor would also wait for the next tile to arrive from HBM.
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef const __attribute__((address_space(4))) v4i ConstV4i;
+
+__device__ __forceinline__ int4 read_const(const int4 *p, int i) {
+    const v4i v = ((ConstV4i *)(p))[i];
+    return int4{v.x, v.y, v.z, v.w};
+}
+
 template <int NV>
 __device__ __forceinline__ void add_vote(uint32_t (&votes)[NV], int cls) {
-    const int word = cls >> 2;
-    const uint32_t inc = 1u << ((cls & 3) * 8);
+    if constexpr (NV == 2) {
+        // eight counters in one 64-bit word: a shift and a 64-bit add
+        uint64_t v = uint64_t(votes[1]) << 32 | votes[0];
+        v += uint64_t(1) << (cls * 8);
+        votes[0] = uint32_t(v);
+        votes[1] = uint32_t(v >> 32);
+    } else {
+        const int word = cls >> 2;
+        const uint32_t inc = 1u << ((cls & 3) * 8);
 #pragma unroll
-    for (int r = 0; r < NV; ++r) votes[r] += (word == r) ? inc : 0u;
+        for (int r = 0; r < NV; ++r) votes[r] += (word == r) ? inc : 0u;
+    }
 }
 
 // Class with the most votes; the strict comparison keeps the smallest id on ties.
@@ -49,11 +69,19 @@ __device__ __forceinline__ int majority(const uint32_t (&votes)[NV], int n_class
 // Trees walked together per lane by the data decomposition.
 constexpr int kIlp = 4;
 
+// The whole chunk buffer, copied by the workgroup.
+__device__ __forceinline__ void copy_chunk(const FArgs &a, int4 *tab, const int4 &ch) {
+    const int4 *src = a.tables + (ch.z >> 4);
+    for (int i = threadIdx.x; i < (ch.w >> 4); i += blockDim.x) tab[i] = src[i];
+}
+
 // SD = 0: data decomposition; SD > 0: speculative decomposition with window depth SD.
 template <int RS, int LOAD, bool TAB_LDS, int NV, int SD>
-__global__ void __launch_bounds__(512) forest_kernel(FArgs a) {
+__global__ void __launch_bounds__(64 * forest_max_waves(SD == 0 ? 0 : 1, SD, RS)) forest_kernel(FArgs a) {
     extern __shared__ int4 lds[];
-    constexpr bool kPrefetch = LOAD != kLoadScalar && RS <= 32;   // compute-bound: wide rows unprefetched
+    // compute-bound: wide rows unprefetched; the speculative walk with vector loads keeps
+    // no prefetch either (its registers would not fit 16 wavefronts per CU)
+    constexpr bool kPrefetch = LOAD != kLoadScalar && RS <= 32 && !(SD > 0 && LOAD == kLoadVec);
     const int wave = threadIdx.x >> 6;
     const int lane = threadIdx.x & 63;
     float *tile = reinterpret_cast<float *>(lds) + wave * (kTileRows * RS);
@@ -78,6 +106,15 @@ __global__ void __launch_bounds__(512) forest_kernel(FArgs a) {
             return spec.run(sl, ex, levels, root, tile);
         }
     };
+
+    // A forest whose tables form one chunk is copied once: the tables then stay for every
+    // group.  Otherwise the chunks are copied in turn for each group.
+    if constexpr (TAB_LDS) {
+        if (a.n_chunks == 1) {
+            copy_chunk(a, tab, read_const(a.chunks, 0));
+            __syncthreads();
+        }
+    }
 
     // Full tiles are prefetched one group ahead; the partial last tile is staged directly.
     const int64_t n_full = a.in.n / kTileRows;
@@ -107,12 +144,13 @@ __global__ void __launch_bounds__(512) forest_kernel(FArgs a) {
 #pragma unroll
         for (int r = 0; r < NV; ++r) votes[r] = 0u;
         for (int c = 0; c < a.n_chunks; ++c) {
-            const int4 ch = a.chunks[c];             // {first, end, byte_off, bytes}
+            const int4 ch = read_const(a.chunks, c);             // {first, end, byte_off, bytes}
             if constexpr (TAB_LDS) {
-                __syncthreads();                     // previous chunk no longer read
-                const int4 *src = a.tables + (ch.z >> 4);
-                for (int i = threadIdx.x; i < (ch.w >> 4); i += blockDim.x) tab[i] = src[i];
-                __syncthreads();
+                if (a.n_chunks > 1) {
+                    __syncthreads();                 // previous chunk no longer read
+                    copy_chunk(a, tab, ch);
+                    __syncthreads();
+                }
                 if (active) {
                     const char *cbase = reinterpret_cast<const char *>(tab);
                     int k = ch.x;
@@ -123,7 +161,7 @@ __global__ void __launch_bounds__(512) forest_kernel(FArgs a) {
                             int32_t code[kIlp];
 #pragma unroll
                             for (int i = 0; i < kIlp; ++i) {
-                                const int4 d = a.trees[k + i];
+                                const int4 d = read_const(a.trees, k + i);
                                 base[i] = cbase + (d.x - ch.z);
                                 sb[i] = d.y;
                                 lv[i] = d.z;
@@ -133,8 +171,26 @@ __global__ void __launch_bounds__(512) forest_kernel(FArgs a) {
                             for (int i = 0; i < kIlp; ++i) add_vote(votes, ~code[i]);
                         }
                     }
+                    if constexpr (SD == 0) {
+                        if (k + 2 <= ch.y) {
+                            const char *base[2];
+                            int sb[2], lv[2];
+                            int32_t code[2];
+#pragma unroll
+                            for (int i = 0; i < 2; ++i) {
+                                const int4 d = read_const(a.trees, k + i);
+                                base[i] = cbase + (d.x - ch.z);
+                                sb[i] = d.y;
+                                lv[i] = d.z;
+                            }
+                            dev::walk_data_k<2, kStride>(base, sb, lv, a.depth, row, sw, code);
+                            add_vote(votes, ~code[0]);
+                            add_vote(votes, ~code[1]);
+                            k += 2;
+                        }
+                    }
                     for (; k < ch.y; ++k) {
-                        const int4 d = a.trees[k];   // {byte_off, slot_bytes, levels, 0}
+                        const int4 d = read_const(a.trees, k);   // {byte_off, slot_bytes, levels, 0}
                         add_vote(votes, ~eval_tree(cbase + (d.x - ch.z), d.z, d.y));
                     }
                 }
@@ -149,7 +205,7 @@ __global__ void __launch_bounds__(512) forest_kernel(FArgs a) {
                             int32_t code[kIlp];
 #pragma unroll
                             for (int i = 0; i < kIlp; ++i) {
-                                const int4 d = a.trees[k + i];
+                                const int4 d = read_const(a.trees, k + i);
                                 base[i] = gbase + d.x;
                                 sb[i] = d.y;
                                 lv[i] = d.z;
@@ -160,7 +216,7 @@ __global__ void __launch_bounds__(512) forest_kernel(FArgs a) {
                         }
                     }
                     for (; k < ch.y; ++k) {
-                        const int4 d = a.trees[k];
+                        const int4 d = read_const(a.trees, k);
                         add_vote(votes, ~eval_tree(gbase + d.x, d.z, d.y));
                     }
                 }

@@ -9,7 +9,16 @@ namespace dtree {
 
 constexpr int kTileRows = 64;          // records per wavefront tile (one per lane)
 constexpr int kMaxRowStride = 256;     // LDS row stride limit in floats (n_features <= 256)
-constexpr int kMaxWavesPerBlock = 8;   // kernels are built for <= 512 threads
+constexpr int kMaxWavesPerBlock = 8;   // kernels are built for <= 512 threads, except:
+// forest instances whose registers fit 16 wavefronts per CU without spilling (data walk
+// on rows of up to 128 features, speculative walk with depth-2 windows on rows of up to
+// 32), built for <= 1024.  `depth` is the speculative window depth (unused for data).
+constexpr int kMaxForestWavesPerBlock = 16;
+__host__ __device__ constexpr int forest_max_waves(int algo, int depth, int row_stride) {
+    return (algo == 0 ? row_stride <= 128 : depth == 2 && row_stride <= 32)
+               ? kMaxForestWavesPerBlock
+               : kMaxWavesPerBlock;
+}
 constexpr int kMaxForestTrees = 255;   // 8-bit vote counters
 constexpr int kMaxForestClasses = 64;  // 16 VGPRs of packed counters
 
