@@ -505,24 +505,60 @@ struct Spec {
         return p - S;
     }
 
+    // Windows of 2 or 4 slots have all their exits in one 8- or 16-byte word: a lane
+    // reads its record's exits together with the slot reads of the level, so the exit is
+    // picked from registers once the bits are walked instead of read after the walk.
+    static constexpr bool kExitWord = S == 2 || S == 4;
+    typedef int32_t ExitWord __attribute__((ext_vector_type(S == 4 ? 4 : 2)));
+
+    static __device__ __forceinline__ int32_t pick(const ExitWord &e, int i) {
+        if constexpr (S == 4) {
+            const int32_t lo = (i & 1) ? e.y : e.x;
+            const int32_t hi = (i & 1) ? e.w : e.z;
+            return (i & 2) ? hi : lo;
+        } else {
+            return (i & 1) ? e.y : e.x;
+        }
+    }
+
     // Exit code of every lane's record.  `root` = slots[j] of window 0.  All 64 lanes
     // must be active.
     __device__ __forceinline__ int32_t run(const Slot *slots, const int32_t *exits, int levels,
                                            const Slot &root, const T *tile) const {
-        int w = 0;
-        int32_t code = exits[walk(eval(slots, true, root, 0, tile))];
-        bool done = code < 0;
-        if (!done) w = code;
-        for (int level = 1; level < levels; ++level) {
-            if (__all(done)) break;
-            const Bits bits = eval(slots, false, root, w, tile);
-            if (!done) {
-                code = exits[(w << D) + walk(bits)];
-                done = code < 0;
-                if (!done) w = code;
+        if constexpr (kExitWord) {
+            const ExitWord *ew = reinterpret_cast<const ExitWord *>(exits);
+            int w = 0;
+            const ExitWord e0 = ew[0];
+            int32_t code = pick(e0, walk(eval(slots, true, root, 0, tile)));
+            bool done = code < 0;
+            if (!done) w = code;
+            for (int level = 1; level < levels; ++level) {
+                if (__all(done)) break;
+                const ExitWord e = ew[w];       // w stays a valid window once done
+                const Bits bits = eval(slots, false, root, w, tile);
+                if (!done) {
+                    code = pick(e, walk(bits));
+                    done = code < 0;
+                    if (!done) w = code;
+                }
             }
+            return code;
+        } else {
+            int w = 0;
+            int32_t code = exits[walk(eval(slots, true, root, 0, tile))];
+            bool done = code < 0;
+            if (!done) w = code;
+            for (int level = 1; level < levels; ++level) {
+                if (__all(done)) break;
+                const Bits bits = eval(slots, false, root, w, tile);
+                if (!done) {
+                    code = exits[(w << D) + walk(bits)];
+                    done = code < 0;
+                    if (!done) w = code;
+                }
+            }
+            return code;
         }
-        return code;
     }
 };
 
