@@ -75,6 +75,31 @@ __device__ __forceinline__ void copy_chunk(const FArgs &a, int4 *tab, const int4
     for (int i = threadIdx.x; i < (ch.w >> 4); i += blockDim.x) tab[i] = src[i];
 }
 
+// Chunks of up to kStage * 16 bytes per thread are loaded into registers before the
+// barrier that frees the chunk buffer, so the loads' latency overlaps the wait for the
+// slowest wavefront; only the LDS writes sit between the two barriers.
+constexpr int kStage = 2;
+
+__device__ __forceinline__ void copy_chunk_staged(const FArgs &a, int4 *tab, const int4 &ch) {
+    const v4i *src = reinterpret_cast<const v4i *>(a.tables) + (ch.z >> 4);
+    v4i *dst = reinterpret_cast<v4i *>(tab);
+    const int n16 = ch.w >> 4;                       // >= 1: a chunk holds a tree
+    v4i v[kStage];
+#pragma unroll
+    for (int q = 0; q < kStage; ++q) {
+        // unconditional loads (a thread past the end re-reads the last word): no branch
+        // between the loads, so they are all in flight before the barrier
+        const int i = int(threadIdx.x) + q * int(blockDim.x);
+        v[q] = src[i < n16 ? i : n16 - 1];
+    }
+    __syncthreads();                                 // previous chunk no longer read
+#pragma unroll
+    for (int q = 0; q < kStage; ++q) {
+        const int i = int(threadIdx.x) + q * int(blockDim.x);
+        if (i < n16) dst[i] = v[q];
+    }
+}
+
 // SD = 0: data decomposition; SD > 0: speculative decomposition with window depth SD.
 template <int RS, int LOAD, bool TAB_LDS, int NV, int SD>
 __global__ void __launch_bounds__(64 * forest_max_waves(SD == 0 ? 0 : 1, SD, RS)) forest_kernel(FArgs a) {
@@ -115,6 +140,7 @@ __global__ void __launch_bounds__(64 * forest_max_waves(SD == 0 ? 0 : 1, SD, RS)
             __syncthreads();
         }
     }
+    const bool staged = a.table_lds_bytes <= kStage * 16 * int(blockDim.x);
 
     // Full tiles are prefetched one group ahead; the partial last tile is staged directly.
     const int64_t n_full = a.in.n / kTileRows;
@@ -147,8 +173,12 @@ __global__ void __launch_bounds__(64 * forest_max_waves(SD == 0 ? 0 : 1, SD, RS)
             const int4 ch = read_const(a.chunks, c);             // {first, end, byte_off, bytes}
             if constexpr (TAB_LDS) {
                 if (a.n_chunks > 1) {
-                    __syncthreads();                 // previous chunk no longer read
-                    copy_chunk(a, tab, ch);
+                    if (staged) {
+                        copy_chunk_staged(a, tab, ch);
+                    } else {
+                        __syncthreads();             // previous chunk no longer read
+                        copy_chunk(a, tab, ch);
+                    }
                     __syncthreads();
                 }
                 if (active) {
