@@ -76,6 +76,23 @@ def test_tree_counts_and_shapes(dt, n_trees):
     _check(dt, nodes, off, x, 19, 7)
 
 
+@pytest.mark.parametrize("F", [20, 100, 200])
+@pytest.mark.parametrize("spec_depth", [2, 4])
+def test_row_widths_and_window_depths(dt, F, spec_depth):
+    """Rows of 20, 100 and 200 features (vector and scalar loads; 16- and 8-wavefront
+    workgroups) with several tree chunks per pass, both speculative window depths."""
+    r = np.random.Generator(np.random.PCG64(F * 10 + spec_depth))
+    trees = [W.complete_tree(r, int(r.integers(6, 10)), F, 11) for _ in range(40)]
+    nodes, off = _forest(trees)
+    x = W.uniform_f32(r, (6001, F))
+    want = oracle.forest_classes(nodes, off, x, F, 11)
+    f = dt.Forest(nodes, off, F, 11, spec_window_depth=spec_depth)
+    xd = torch.from_numpy(x).cuda()
+    for algo in ALGOS:
+        got = f.classify(xd, algo=algo, out_kind="class_i32").cpu().numpy()
+        np.testing.assert_array_equal(got, want, err_msg=algo)
+
+
 def test_large_trees_read_tables_in_place(dt):
     """Trees whose tables do not fit the LDS: the forest reads them from global memory."""
     r = np.random.Generator(np.random.PCG64(7))
