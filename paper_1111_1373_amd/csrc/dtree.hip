@@ -185,15 +185,16 @@ std::vector<const void *> g_prepared;
 // Wavefronts per CU the library aims for (measured on MI355X).  The data decomposition is
 // HBM-bound once about 64 KiB of record tiles are in flight per CU; more wavefronts only
 // add contention.  The speculative decomposition, which does 2^D times the lane work per
-// record, needs 8 wavefronts per CU to hide its LDS latency on narrow tiles, but with
-// 16 KiB tiles (64 fp32 features) 64 KiB in flight is again the better point: 4
-// wavefronts keep a larger result buffer next to the tables and measure 640 us on
-// 16,777,216 x 64 records against 674 us with 5.  The path reduction is latency-bound
+// record, is bound by LDS latency once the tiles are small, and then gains from every
+// wavefront up to 16 per CU (uint8 records of 64 features: 207 us with 16 against 282 us
+// with 8); with 16 KiB tiles (64 fp32 features) 64 KiB in flight is again the better
+// point: 4 wavefronts keep a larger result buffer next to the tables and measure 640 us
+// on 16,777,216 x 64 records against 674 us with 5.  The path reduction is latency-bound
 // and takes as many wavefronts as fit, up to 8.
 int target_waves_per_cu(int algo, int tile_bytes) {
     const int hbm = std::max(2, std::min(32, (64 * 1024) / tile_bytes));
     if (algo == DT_ALGO_DATA) return hbm;
-    if (algo == DT_ALGO_SPECULATIVE) return std::min(8, hbm);
+    if (algo == DT_ALGO_SPECULATIVE) return std::min(16, hbm);
     return 8;
 }
 
