@@ -318,10 +318,11 @@ __device__ __forceinline__ void stage_now(const Rows &in, float *tile, int64_t t
 // of p are fetched as one 16-byte pair and the comparison selects between them, so each
 // level costs one LDS round trip instead of two dependent ones.
 // `row[(f ^ sw) * STRIDE]` is feature f of this lane's record: STRIDE 1 for row-major
-// tiles, kTileRows (and sw = 0) for column-major ones.
-template <int XT, int STRIDE = 1>
+// tiles, kTileRows (and sw = 0) for column-major ones.  Exit codes are EX: int32, or int16
+// where a forest's codes all fit (sign-extended when read).
+template <int XT, int STRIDE = 1, class EX = int32_t>
 __device__ __forceinline__ int32_t walk_data(const typename Node<XT>::S *slots,
-                                             const int32_t *exits, int D, int levels,
+                                             const EX *exits, int D, int levels,
                                              const typename Elem<XT>::T *row, int sw) {
     using N = Node<XT>;
     using NS = typename N::S;
@@ -342,7 +343,7 @@ __device__ __forceinline__ int32_t walk_data(const typename Node<XT>::S *slots,
         }
         const auto xv = row[(N::feature(s) ^ sw) * STRIDE];
         p = 2 * p + int(N::right(xv, s));
-        code = exits[(w << D) + p - S];
+        code = int32_t(exits[(w << D) + p - S]);
         if (code < 0) break;
         w = code;
     }
@@ -352,7 +353,7 @@ __device__ __forceinline__ int32_t walk_data(const typename Node<XT>::S *slots,
 // Data decomposition over K trees at once (forests): the K walks of one record are
 // independent, so interleaving them keeps K LDS dependency chains in flight per lane.
 // Tree i's tables start at base[i]; all trees share the window depth D.
-template <int K, int STRIDE = 1>
+template <int K, int STRIDE = 1, class EX = int32_t>
 __device__ __forceinline__ void walk_data_k(const char *const (&base)[K], const int (&slot_bytes)[K],
                                             const int (&levels)[K], int D, const float *row,
                                             int sw, int32_t (&code)[K]) {
@@ -389,7 +390,7 @@ __device__ __forceinline__ void walk_data_k(const char *const (&base)[K], const 
         int32_t c[K];
 #pragma unroll
         for (int i = 0; i < K; ++i)
-            c[i] = reinterpret_cast<const int32_t *>(base[i] + slot_bytes[i])[(w[i] << D) + p[i] - S];
+            c[i] = int32_t(reinterpret_cast<const EX *>(base[i] + slot_bytes[i])[(w[i] << D) + p[i] - S]);
         bool all_done = true;
 #pragma unroll
         for (int i = 0; i < K; ++i) {
@@ -505,39 +506,57 @@ struct Spec {
         return p - S;
     }
 
-    // Windows of 2 or 4 slots have all their exits in one 8- or 16-byte word: a lane
+    // Windows of 2 or 4 slots have all their exits in one 4- to 16-byte word: a lane
     // reads its record's exits together with the slot reads of the level, so the exit is
     // picked from registers once the bits are walked instead of read after the walk.
+    // Exit codes are EX: int32, or int16 where a forest's codes all fit.
     static constexpr bool kExitWord = S == 2 || S == 4;
-    typedef int32_t ExitWord __attribute__((ext_vector_type(S == 4 ? 4 : 2)));
+    typedef int32_t ExitWord32 __attribute__((ext_vector_type(S == 4 ? 4 : 2)));
+    template <class EX>
+    using ExitWord = typename std::conditional<
+        sizeof(EX) == 4, ExitWord32,
+        typename std::conditional<S == 4, uint2, uint32_t>::type>::type;
 
-    static __device__ __forceinline__ int32_t pick(const ExitWord &e, int i) {
-        if constexpr (S == 4) {
-            const int32_t lo = (i & 1) ? e.y : e.x;
-            const int32_t hi = (i & 1) ? e.w : e.z;
-            return (i & 2) ? hi : lo;
+    template <class EX>
+    static __device__ __forceinline__ int32_t pick(const ExitWord<EX> &e, int i) {
+        if constexpr (sizeof(EX) == 4) {
+            if constexpr (S == 4) {
+                const int32_t lo = (i & 1) ? e.y : e.x;
+                const int32_t hi = (i & 1) ? e.w : e.z;
+                return (i & 2) ? hi : lo;
+            } else {
+                return (i & 1) ? e.y : e.x;
+            }
         } else {
-            return (i & 1) ? e.y : e.x;
+            // int16 codes, two per 32-bit word, code 2k + h in bits [16h, 16h + 16)
+            uint32_t word;
+            if constexpr (S == 4)
+                word = (i & 2) ? e.y : e.x;
+            else
+                word = e;
+            return int32_t(word << (16 - 16 * (i & 1))) >> 16;
         }
     }
 
     // Exit code of every lane's record.  `root` = slots[j] of window 0.  All 64 lanes
     // must be active.
-    __device__ __forceinline__ int32_t run(const Slot *slots, const int32_t *exits, int levels,
+    template <class EX = int32_t>
+    __device__ __forceinline__ int32_t run(const Slot *slots, const EX *exits, int levels,
                                            const Slot &root, const T *tile) const {
         if constexpr (kExitWord) {
-            const ExitWord *ew = reinterpret_cast<const ExitWord *>(exits);
+            using EW = ExitWord<EX>;
+            const EW *ew = reinterpret_cast<const EW *>(exits);
             int w = 0;
-            const ExitWord e0 = ew[0];
-            int32_t code = pick(e0, walk(eval(slots, true, root, 0, tile)));
+            const EW e0 = ew[0];
+            int32_t code = pick<EX>(e0, walk(eval(slots, true, root, 0, tile)));
             bool done = code < 0;
             if (!done) w = code;
             for (int level = 1; level < levels; ++level) {
                 if (__all(done)) break;
-                const ExitWord e = ew[w];       // w stays a valid window once done
+                const EW e = ew[w];             // w stays a valid window once done
                 const Bits bits = eval(slots, false, root, w, tile);
                 if (!done) {
-                    code = pick(e, walk(bits));
+                    code = pick<EX>(e, walk(bits));
                     done = code < 0;
                     if (!done) w = code;
                 }
@@ -545,14 +564,14 @@ struct Spec {
             return code;
         } else {
             int w = 0;
-            int32_t code = exits[walk(eval(slots, true, root, 0, tile))];
+            int32_t code = int32_t(exits[walk(eval(slots, true, root, 0, tile))]);
             bool done = code < 0;
             if (!done) w = code;
             for (int level = 1; level < levels; ++level) {
                 if (__all(done)) break;
                 const Bits bits = eval(slots, false, root, w, tile);
                 if (!done) {
-                    code = exits[(w << D) + walk(bits)];
+                    code = int32_t(exits[(w << D) + walk(bits)]);
                     done = code < 0;
                     if (!done) w = code;
                 }

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdint>
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -321,6 +322,7 @@ struct ForestEncoding {
     int64_t max_tree_bytes = 0;
     int32_t chunk_lds_bytes = 0; // LDS reserved for one chunk (0: tables read in place)
     int32_t waves = 0;           // wavefronts per workgroup (one tile each)
+    bool exit16 = false;         // exit codes stored as int16
 };
 
 void free_forest_encoding(ForestEncoding *e) {
@@ -501,17 +503,29 @@ int vote_words_for(int32_t n_classes) {
 
 // Encode every tree with window depth `depth` and lay the tables out back to back.
 void encode_forest(const dt_node *nodes, const int32_t *offsets, int32_t n_trees,
-                   const std::vector<dtree::TreeShape> &shapes, int depth,
+                   const std::vector<dtree::TreeShape> &shapes, int algo, int depth,
                    std::vector<unsigned char> *bytes, ForestEncoding *enc) {
     enc->depth = depth;
     enc->trees.assign(size_t(n_trees), int4{0, 0, 0, 0});
     enc->max_tree_bytes = 0;
     bytes->clear();
+    std::vector<dtree::WindowTables> wts(static_cast<size_t>(n_trees));
+    // Exit codes (next window ids, and results -(class + 1)) of the data decomposition are
+    // stored as int16 when every code of the forest fits: a third less table per tree, so
+    // more trees share a chunk.  (The speculative walk keeps int32 codes: its int16
+    // instance needs more registers than 16 wavefronts per CU leave it.)
+    bool fits16 = algo == DT_ALGO_DATA;
     for (int32_t k = 0; k < n_trees; ++k) {
-        dtree::WindowTables wt;
-        dtree::build_windows(nodes + offsets[k], shapes[size_t(k)], depth, &wt);
+        dtree::build_windows(nodes + offsets[k], shapes[size_t(k)], depth, &wts[size_t(k)]);
+        for (int32_t c : wts[size_t(k)].exit_class)
+            fits16 = fits16 && c >= INT16_MIN && c <= INT16_MAX;
+    }
+    enc->exit16 = fits16;
+    const int64_t exit_size = fits16 ? 2 : 4;
+    for (int32_t k = 0; k < n_trees; ++k) {
+        const dtree::WindowTables &wt = wts[size_t(k)];
         const int64_t n_slots = int64_t(wt.n_windows) * wt.slots;
-        const int64_t sb = align16(n_slots * 8), eb = align16(n_slots * 4);
+        const int64_t sb = align16(n_slots * 8), eb = align16(n_slots * exit_size);
         const int64_t off = int64_t(bytes->size());
         bytes->resize(size_t(off + sb + eb), 0);
         unsigned char *p = bytes->data() + off;
@@ -519,7 +533,14 @@ void encode_forest(const dt_node *nodes, const int32_t *offsets, int32_t n_trees
             std::memcpy(p + 8 * i, &wt.threshold[size_t(i)], 4);
             std::memcpy(p + 8 * i + 4, &wt.feature[size_t(i)], 4);
         }
-        std::memcpy(p + sb, wt.exit_class.data(), size_t(n_slots * 4));
+        if (fits16) {
+            for (int64_t i = 0; i < n_slots; ++i) {
+                const int16_t c = int16_t(wt.exit_class[size_t(i)]);
+                std::memcpy(p + sb + 2 * i, &c, 2);
+            }
+        } else {
+            std::memcpy(p + sb, wt.exit_class.data(), size_t(n_slots * 4));
+        }
         enc->trees[size_t(k)] = int4{int(off), int(sb), wt.levels, 0};
         enc->max_tree_bytes = std::max(enc->max_tree_bytes, sb + eb);
     }
@@ -611,7 +632,7 @@ dt_status plan_forest(const DeviceCaps &caps, int algo, int row_stride, int load
                       int vote_words, const ForestEncoding &enc, Plan *plan) {
     const bool tab_lds = enc.chunk_lds_bytes > 0;
     plan->fn = dtree::forest_kernel_for(algo, row_stride, load_mode, tab_lds, vote_words,
-                                        enc.depth);
+                                        enc.depth, enc.exit16);
     if (!plan->fn) {
         plan->why = "no forest kernel instance for this configuration";
         return plan->status = DT_ERR_UNSUPPORTED;
@@ -718,7 +739,7 @@ dt_status forest_create_impl(const dt_node *nodes, const int32_t *offsets, int32
     const int depth[2] = {data_d, spec_d};
     for (int algo = 0; algo < 2; ++algo) {
         std::vector<unsigned char> bytes;
-        encode_forest(nodes, offsets, n_trees, shapes, depth[algo], &bytes, &f->enc[algo]);
+        encode_forest(nodes, offsets, n_trees, shapes, algo, depth[algo], &bytes, &f->enc[algo]);
         if (f->row_stride <= dtree::kMaxRowStride)
             chunk_forest(f->caps, algo, f->row_stride, opt ? opt->waves_per_cu : 0,
                          &f->enc[algo]);

@@ -63,8 +63,8 @@ constexpr int kPathIntsPerWave = 128;
 __host__ __device__ inline int out_buffer_bytes(int cap, int out_bytes) { return cap * kTileRows * out_bytes; }
 
 // Forest kernel arguments.  Tree k's tables are the bytes [off_k, off_k + slot_bytes_k)
-// (slots) followed by its exit codes, inside `tables`; trees[k] = {off_k, slot_bytes_k,
-// levels_k, 0}.  Chunks are runs of consecutive trees staged into the LDS together:
+// (slots) followed by its exit codes (int16 when every code of the forest fits, else
+// int32), inside `tables`; trees[k] = {off_k, slot_bytes_k, levels_k, 0}.  Chunks are runs of consecutive trees staged into the LDS together:
 // chunks[c] = {first_tree, end_tree, byte_off, bytes}.
 struct FArgs {
     Rows in;
@@ -108,9 +108,12 @@ const void *kernel_for_u8(int algo, int row_stride, int load_mode, bool tables_i
 const void *path_kernel_for(int row_stride, int load_mode, bool tables_in_lds, int depth);
 
 // Forest kernel instance; `vote_words` = 32-bit words of packed 8-bit counters
-// (2, 4 or 16 for up to 8, 16 or 64 classes).
+// (2, 4 or 16 for up to 8, 16 or 64 classes); `exit16`: exit codes stored as int16.
 const void *forest_kernel_for(int algo, int row_stride, int load_mode, bool tables_in_lds,
-                              int vote_words, int depth);
+                              int vote_words, int depth, bool exit16);
+// The int16 instances (their own translation unit).
+const void *forest_kernel_for_ex16(int algo, int row_stride, int load_mode, bool tables_in_lds,
+                                   int vote_words, int depth);
 
 // One-time per-instance setup (raise the dynamic LDS limit to the device maximum).
 hipError_t prepare_kernel(const void *fn, int max_lds_bytes);

@@ -102,6 +102,25 @@ def test_large_trees_read_tables_in_place(dt):
     _check(dt, nodes, off, x, 16, 10)
 
 
+@pytest.mark.parametrize("n_internal", [32768, 32769])
+def test_exit_codes_at_the_int16_limit(dt, n_internal):
+    """Exit codes are stored as int16 when every code of the forest fits, else as int32.  A
+    chain cut into one-node windows has window ids 0 .. n_internal - 1: the largest is 32767
+    (int16) for 32,768 decision nodes and 32768 (int32) for 32,769.  Exits are rare (one
+    record in 10,000 per node), so a few percent of the records travel past window 32,767."""
+    r = np.random.Generator(np.random.PCG64(11))
+    chain = W.chain_tree(r, n_internal, 8, 5, p_exit=1e-4)
+    nodes, off = _forest([chain, W.complete_tree(r, 6, 8, 5)])
+    x = W.uniform_f32(r, (3000, 8))
+    want = oracle.forest_classes(nodes, off, x, 8, 5)
+    f = dt.Forest(nodes, off, 8, 5, data_window_depth=1)
+    got = f.classify(torch.from_numpy(x).cuda(), algo="data", out_kind="class_i32").cpu().numpy()
+    np.testing.assert_array_equal(got, want)
+    # some records reach the last window (its decision node is at depth n_internal - 1, and
+    # the chain's breadth-first ids put its leaves at 2 (n_internal - 1) + 1 and + 2)
+    assert (oracle.tree_leaves(chain, x, 8) >= 2 * (n_internal - 1) + 1).sum() > 10
+
+
 @pytest.mark.parametrize("n", [1, 63, 65, 130, 1000, 70000])
 def test_ragged_sizes_and_strides(dt, n):
     w = W.config(5, n_samples=n)
