@@ -27,6 +27,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0
+# fp32 vector compares (one per lane, not packed): 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz.
+PEAK_COMPARES_T = 256 * 4 * 16 * 2.4e9 / 1e12
 # The paper's kernel times on its CUDA 2.0 GPU (Table 1): speculative 404.466 us vs data
 # 538.235 us (about 25% faster).
 PAPER_CONTEXT = {"speculative_us": 404.466, "data_us": 538.235, "ratio": 404.466 / 538.235,
@@ -68,6 +70,20 @@ def recorded_traffic(workload: str, algo: str):
         return float(kv["hbm_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+def forest_depth_sum(w) -> int:
+    """Sum over the forest's trees of the longest root-to-leaf path: the tree steps (one
+    compare each) of every record when the trees are complete, as in the forest workload."""
+    total = 0
+    for k in range(len(w.tree_offsets) - 1):
+        t = w.nodes[w.tree_offsets[k]:w.tree_offsets[k + 1]]
+        depth = [0] * len(t)
+        for i in range(len(t)):          # children follow their parent in the array
+            if t["cls"][i] < 0:
+                depth[t["left"][i]] = depth[t["left"][i] + 1] = depth[i] + 1
+        total += max(depth)
+    return total
 
 
 W_NARROW = ("f16", "bf16", "u8")
@@ -486,6 +502,14 @@ def main() -> int:
                      "kernel": r["kernel"]},
         "cpu_baseline": cpu,
         "cpu_baseline_all_cores": cpu_all,
+        # A forest does 32 trees x 10 levels of compare-and-index per 128-byte record: its
+        # bound is the vector ALU and the LDS, not HBM.  One tree step is one fp32 compare.
+        "roofline_alu": ({"bound": "alu", "unit": "T compares/s", "peak": PEAK_COMPARES_T,
+                          "achieved": n * forest_depth_sum(w) / kavg / 1e12,
+                          "frac": n * forest_depth_sum(w) / kavg / 1e12 / PEAK_COMPARES_T,
+                          "compares_per_launch": n * forest_depth_sum(w),
+                          "kernel": r["kernel"]}
+                         if w.is_forest else None),
         "parity": "bit-exact vs oracle on all %d records" % n
                   if all(v["mismatches_vs_oracle"] == 0 for v in results.values()) and
                   (outer is None or
