@@ -121,6 +121,38 @@ def test_exit_codes_at_the_int16_limit(dt, n_internal):
     assert (oracle.tree_leaves(chain, x, 8) >= 2 * (n_internal - 1) + 1).sum() > 10
 
 
+@pytest.mark.parametrize("F", [4, 32, 64, 65])
+def test_special_values_ties_and_near_ties(dt, F):
+    """Records on and around the thresholds of a forest: a quarter of every record's values
+    sit on a threshold or on one of its float neighbours up to 40 steps away, and a few
+    are NaN, -0/+0, infinities or denormals, which also appear among the thresholds."""
+    from tests import treeutil as TU
+    r = np.random.Generator(np.random.PCG64(1373 + F))
+    pool = np.concatenate([TU.special_pool(), W.uniform_f32(r, 8), -W.uniform_f32(r, 4),
+                           np.float32([3e-39, -3e-39, 1e30, -1e30])])
+    trees = [W.random_full_tree(r, int(r.integers(1, 120)), F, 6, threshold_values=pool)
+             for _ in range(9)]
+    nodes, off = _forest(trees)
+    internal = nodes["cls"] < 0
+    th = nodes["threshold"][internal]
+    n = 20000
+    x = W.uniform_f32(r, (n, F))
+    # every record: a quarter of its entries on a threshold or a float neighbour of one
+    pick = r.random((n, F)) < 0.25
+    base = th[r.integers(0, len(th), size=int(pick.sum()))]
+    steps = r.integers(-40, 41, size=base.shape)
+    toward = np.where(steps > 0, np.float32(np.inf), np.float32(-np.inf)).astype(np.float32)
+    near = base.copy()
+    with np.errstate(over="ignore", invalid="ignore"):
+        for i in range(1, 41):
+            m = np.abs(steps) >= i
+            near[m] = np.nextafter(near[m], toward[m])
+    x[pick] = near
+    special = r.random((n, F)) < 0.03
+    x[special] = pool[r.integers(0, len(pool), size=int(special.sum()))]
+    _check(dt, nodes, off, x, F, 6)
+
+
 @pytest.mark.parametrize("n", [1, 63, 65, 130, 1000, 70000])
 def test_ragged_sizes_and_strides(dt, n):
     w = W.config(5, n_samples=n)
