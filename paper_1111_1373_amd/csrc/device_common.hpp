@@ -506,49 +506,32 @@ struct Spec {
         return p - S;
     }
 
-    // Windows of 2 or 4 slots have all their exits in one 4- to 16-byte word: a lane
+    // Windows of 2 or 4 slots have all their exits in one 8- or 16-byte word: a lane
     // reads its record's exits together with the slot reads of the level, so the exit is
     // picked from registers once the bits are walked instead of read after the walk.
-    // Exit codes are EX: int32, or int16 where a forest's codes all fit.
     static constexpr bool kExitWord = S == 2 || S == 4;
-    typedef int32_t ExitWord32 __attribute__((ext_vector_type(S == 4 ? 4 : 2)));
-    template <class EX>
-    using ExitWord = typename std::conditional<
-        sizeof(EX) == 4, ExitWord32,
-        typename std::conditional<S == 4, uint2, uint32_t>::type>::type;
+    typedef int32_t ExitWord __attribute__((ext_vector_type(S == 4 ? 4 : 2)));
 
-    template <class EX>
-    static __device__ __forceinline__ int32_t pick(const ExitWord<EX> &e, int i) {
-        if constexpr (sizeof(EX) == 4) {
-            if constexpr (S == 4) {
-                const int32_t lo = (i & 1) ? e.y : e.x;
-                const int32_t hi = (i & 1) ? e.w : e.z;
-                return (i & 2) ? hi : lo;
-            } else {
-                return (i & 1) ? e.y : e.x;
-            }
+    static __device__ __forceinline__ int32_t pick(const ExitWord &e, int i) {
+        if constexpr (S == 4) {
+            const int32_t lo = (i & 1) ? e.y : e.x;
+            const int32_t hi = (i & 1) ? e.w : e.z;
+            return (i & 2) ? hi : lo;
         } else {
-            // int16 codes, two per 32-bit word, code 2k + h in bits [16h, 16h + 16)
-            uint32_t word;
-            if constexpr (S == 4)
-                word = (i & 2) ? e.y : e.x;
-            else
-                word = e;
-            return int32_t(word << (16 - 16 * (i & 1))) >> 16;
+            return (i & 1) ? e.y : e.x;
         }
     }
 
     // Exit code of every lane's record.  `root` = slots[j] of window 0.  All 64 lanes
     // must be active.
-    template <class EX = int32_t>
-    __device__ __forceinline__ int32_t run(const Slot *slots, const EX *exits, int levels,
+    __device__ __forceinline__ int32_t run(const Slot *slots, const int32_t *exits, int levels,
                                            const Slot &root, const T *tile) const {
         if constexpr (kExitWord) {
-            using EW = ExitWord<EX>;
+            using EW = ExitWord;
             const EW *ew = reinterpret_cast<const EW *>(exits);
             int w = 0;
             const EW e0 = ew[0];
-            int32_t code = pick<EX>(e0, walk(eval(slots, true, root, 0, tile)));
+            int32_t code = pick(e0, walk(eval(slots, true, root, 0, tile)));
             bool done = code < 0;
             if (!done) w = code;
             for (int level = 1; level < levels; ++level) {
@@ -556,7 +539,7 @@ struct Spec {
                 const EW e = ew[w];             // w stays a valid window once done
                 const Bits bits = eval(slots, false, root, w, tile);
                 if (!done) {
-                    code = pick<EX>(e, walk(bits));
+                    code = pick(e, walk(bits));
                     done = code < 0;
                     if (!done) w = code;
                 }
@@ -564,14 +547,14 @@ struct Spec {
             return code;
         } else {
             int w = 0;
-            int32_t code = int32_t(exits[walk(eval(slots, true, root, 0, tile))]);
+            int32_t code = exits[walk(eval(slots, true, root, 0, tile))];
             bool done = code < 0;
             if (!done) w = code;
             for (int level = 1; level < levels; ++level) {
                 if (__all(done)) break;
                 const Bits bits = eval(slots, false, root, w, tile);
                 if (!done) {
-                    code = int32_t(exits[(w << D) + walk(bits)]);
+                    code = exits[(w << D) + walk(bits)];
                     done = code < 0;
                     if (!done) w = code;
                 }

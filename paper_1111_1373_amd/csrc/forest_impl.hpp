@@ -132,7 +132,7 @@ __global__ void __launch_bounds__(64 * forest_max_waves(SD == 0 ? 0 : 1, SD, RS)
         } else {
             const dev::Spec<kXF32, RS, SD> spec(lane);
             const Slot root = sl[spec.j];
-            return spec.template run<EX>(sl, ex, levels, root, tile);
+            return spec.run(sl, ex, levels, root, tile);   // int32 codes (EX is int32 here)
         }
     };
 
