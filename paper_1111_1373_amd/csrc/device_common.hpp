@@ -311,6 +311,18 @@ __device__ __forceinline__ void stage_now(const Rows &in, float *tile, int64_t t
     }
 }
 
+// One heap step, p <- 2p + b, as a single add with carry: the compare that produces b
+// leaves it as a wave mask in scalar registers, which v_addc takes as its carry-in, so
+// the step costs one vector instruction instead of a select and a shift-or.  Lanes
+// outside the active mask are not written.
+__device__ __forceinline__ int heap_step(int p, bool b) {
+    const uint64_t m = __ballot(b);
+    int q;
+    uint64_t carry_out;
+    asm("v_addc_co_u32_e64 %0, %1, %2, %2, %3" : "=v"(q), "=s"(carry_out) : "v"(p), "s"(m));
+    return q;
+}
+
 // ---- data decomposition: the record of this lane walks one tree --------------------------
 // Within a window the record descends p <- 2p + !(x[f_p] < t_p) for exactly D steps
 // (Procedure 2's "child + predicate" step on the 1-based heap), then the exit names the next
@@ -338,11 +350,11 @@ __device__ __forceinline__ int32_t walk_data(const typename Node<XT>::S *slots,
             const auto xv = row[(N::feature(s) ^ sw) * STRIDE];
             const Pair kids = *reinterpret_cast<const Pair *>(win + 2 * p);
             const bool right = N::right(xv, s);
-            p = 2 * p + int(right);
+            p = heap_step(p, right);
             s = right ? kids.r : kids.l;
         }
         const auto xv = row[(N::feature(s) ^ sw) * STRIDE];
-        p = 2 * p + int(N::right(xv, s));
+        p = heap_step(p, N::right(xv, s));
         code = int32_t(exits[(w << D) + p - S]);
         if (code < 0) break;
         w = code;
@@ -381,7 +393,7 @@ __device__ __forceinline__ void walk_data_k(const char *const (&base)[K], const 
             for (int i = 0; i < K; ++i) {
                 const Slot s = win[i][p[i]];
                 const float xv = row[(s.f ^ sw) * STRIDE];
-                p[i] = 2 * p[i] + int(!(xv < s.t));
+                p[i] = heap_step(p[i], !(xv < s.t));
             }
         }
         // Every chain reads its exit, finished or not (a finished chain re-walked its last
