@@ -439,25 +439,29 @@ struct Spec {
     // index must then be a compile-time constant.
     static constexpr bool kDpp = S == 2 || S == 4 || S == 16;
 
-    // Window id of record seg_shift + G, held by lane seg_shift + G, in every lane of the
-    // segment.
+    // Value w of lane seg_shift + G (record seg_shift + G's window offset) in every lane of
+    // the segment.  Every source lane is in range and enabled, so no old value is needed.
     template <int G>
     __device__ __forceinline__ int window_of(int w) const {
         if constexpr (S == 16)
-            return __builtin_amdgcn_update_dpp(0, w, 0x150 + G, 0xF, 0xF, false);   // row_share
+            return __builtin_amdgcn_mov_dpp(w, 0x150 + G, 0xF, 0xF, true);   // row_share
         else if constexpr (S == 4)
-            return __builtin_amdgcn_update_dpp(0, w, G * 0x55, 0xF, 0xF, false);    // quad_perm
+            return __builtin_amdgcn_mov_dpp(w, G * 0x55, 0xF, 0xF, true);    // quad_perm
         else   // S == 2: quad_perm [G, G, 2 + G, 2 + G]
-            return __builtin_amdgcn_update_dpp(0, w, G | G << 2 | (2 + G) << 4 | (2 + G) << 6,
-                                               0xF, 0xF, false);
+            return __builtin_amdgcn_mov_dpp(w, G | G << 2 | (2 + G) << 4 | (2 + G) << 6,
+                                            0xF, 0xF, true);
     }
 
     // Round g: the segment starting at lane b evaluates record b + g, so record r's bits
     // arrive in r's own segment in the round g == r % S.
-    __device__ __forceinline__ void round(int g, int wr, Bits &bits, const Slot *slots, bool first,
+    __device__ __forceinline__ void round(int g, int wb, Bits &bits, const Slot *slots, bool first,
                                           const Slot &root, const T *tile) const {
         const int r = seg_shift + g;
-        const Slot p = first ? root : slots[(wr << D) + j];
+        // wb: byte offset of record r's window, window id * 2^D * sizeof(Slot); adding it to
+        // this lane's own slot address folds into the broadcast (one DPP add per round)
+        const Slot p = first ? root
+                             : *reinterpret_cast<const Slot *>(
+                                   reinterpret_cast<const char *>(slots + j) + wb);
         const T xv = tile[r * RS + (N::feature(p) ^ swz_el<XT, RS>(r))];
         const uint64_t m = __ballot(N::right(xv, p));
         if (j == g) bits = Bits(m >> seg_shift);
@@ -469,7 +473,8 @@ struct Spec {
     __device__ __forceinline__ void eval_dpp(std::integer_sequence<int, G...>, Bits &bits,
                                              const Slot *slots, bool first, const Slot &root,
                                              int w, const T *tile) const {
-        (round(G0 + G, first ? 0 : window_of<G0 + G>(w), bits, slots, first, root, tile), ...);
+        (round(G0 + G, first ? 0 : window_of<G0 + G>(w * int(sizeof(Slot) << D)), bits, slots,
+               first, root, tile), ...);
         __builtin_amdgcn_sched_barrier(0);
     }
 
@@ -499,10 +504,11 @@ struct Spec {
             for (int g = 0; g < S; ++g) {
                 int wr = 0;
                 if (!first) {
+                    const int wb = w * int(sizeof(Slot) << D);
                     if constexpr (S == 64)
-                        wr = __builtin_amdgcn_readlane(w, g);
+                        wr = __builtin_amdgcn_readlane(wb, g);
                     else
-                        wr = __shfl(w, seg_shift + g);
+                        wr = __shfl(wb, seg_shift + g);
                 }
                 round(g, wr, bits, slots, first, root, tile);
             }
