@@ -29,7 +29,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 struct alignas(8) Slot {
     float t;
-    int32_t f;
+    int32_t f;   // byte offset of the feature in an fp32 row: 4 * feature index
 };
 
 // The two children 2p, 2p+1 of a heap slot: one aligned 16-byte LDS read.
@@ -84,7 +84,7 @@ template <int XT> struct Node;
 template <> struct Node<kXF32> {
     using S = Slot;
     using Pair = Slot2;
-    static __device__ __forceinline__ int feature(const Slot &s) { return s.f; }
+    static __device__ __forceinline__ int feature(const Slot &s) { return s.f >> 2; }
     static __device__ __forceinline__ bool right(float x, const Slot &s) { return !(x < s.t); }
 };
 template <> struct Node<kXF16> {
@@ -111,6 +111,18 @@ template <> struct Node<kXU8> {
         return uint32_t(x) >= (s & 0xFFFFu);
     }
 };
+
+// Feature of slot `s` in a record row of the tile: element (feature ^ sw) * STRIDE of `row`.
+// fp32 slots carry the feature as a byte offset, so the address is one xor-add.
+template <int XT, int STRIDE>
+__device__ __forceinline__ typename Elem<XT>::T feature_at(const typename Elem<XT>::T *row,
+                                                           const typename Node<XT>::S &s, int sw) {
+    if constexpr (XT == kXF32)
+        return *reinterpret_cast<const float *>(reinterpret_cast<const char *>(row) +
+                                                (s.f ^ (sw << 2)) * STRIDE);
+    else
+        return row[(Node<XT>::feature(s) ^ sw) * STRIDE];
+}
 
 // Element-level position swizzle for rows of RS elements of type XT: the word swizzle,
 // scaled to elements (the position of an element within its word is unchanged).
@@ -347,13 +359,13 @@ __device__ __forceinline__ int32_t walk_data(const typename Node<XT>::S *slots,
         int p = 1;
         NS s = win[1];
         for (int k = 1; k < D; ++k) {
-            const auto xv = row[(N::feature(s) ^ sw) * STRIDE];
+            const auto xv = feature_at<XT, STRIDE>(row, s, sw);
             const Pair kids = *reinterpret_cast<const Pair *>(win + 2 * p);
             const bool right = N::right(xv, s);
             p = heap_step(p, right);
             s = right ? kids.r : kids.l;
         }
-        const auto xv = row[(N::feature(s) ^ sw) * STRIDE];
+        const auto xv = feature_at<XT, STRIDE>(row, s, sw);
         p = heap_step(p, N::right(xv, s));
         code = int32_t(exits[(w << D) + p - S]);
         if (code < 0) break;
@@ -392,7 +404,7 @@ __device__ __forceinline__ void walk_data_k(const char *const (&base)[K], const 
 #pragma unroll
             for (int i = 0; i < K; ++i) {
                 const Slot s = win[i][p[i]];
-                const float xv = row[(s.f ^ sw) * STRIDE];
+                const float xv = feature_at<kXF32, STRIDE>(row, s, sw);
                 p[i] = heap_step(p[i], !(xv < s.t));
             }
         }
@@ -462,7 +474,7 @@ struct Spec {
         const Slot p = first ? root
                              : *reinterpret_cast<const Slot *>(
                                    reinterpret_cast<const char *>(slots + j) + wb);
-        const T xv = tile[r * RS + (N::feature(p) ^ swz_el<XT, RS>(r))];
+        const T xv = feature_at<XT, 1>(tile + r * RS, p, swz_el<XT, RS>(r));
         const uint64_t m = __ballot(N::right(xv, p));
         if (j == g) bits = Bits(m >> seg_shift);
     }

@@ -87,8 +87,9 @@ dt_status upload_encoding(const dtree::WindowTables &wt, Encoding *enc) {
     }
     std::vector<unsigned char> host(size_t(total), 0);
     for (int64_t i = 0; i < n_slots; ++i) {
+        const int32_t fb = 4 * wt.feature[size_t(i)];   // byte offset in an fp32 row
         std::memcpy(&host[size_t(8 * i)], &wt.threshold[size_t(i)], 4);
-        std::memcpy(&host[size_t(8 * i + 4)], &wt.feature[size_t(i)], 4);
+        std::memcpy(&host[size_t(8 * i + 4)], &fb, 4);
     }
     const int64_t exit_off = enc->slot_bytes[dtree::kXF32];
     std::memcpy(&host[size_t(exit_off)], wt.exit_class.data(), size_t(n_slots * 4));
@@ -530,8 +531,9 @@ void encode_forest(const dt_node *nodes, const int32_t *offsets, int32_t n_trees
         bytes->resize(size_t(off + sb + eb), 0);
         unsigned char *p = bytes->data() + off;
         for (int64_t i = 0; i < n_slots; ++i) {
+            const int32_t fb = 4 * wt.feature[size_t(i)];   // byte offset in an fp32 row
             std::memcpy(p + 8 * i, &wt.threshold[size_t(i)], 4);
-            std::memcpy(p + 8 * i + 4, &wt.feature[size_t(i)], 4);
+            std::memcpy(p + 8 * i + 4, &fb, 4);
         }
         if (fits16) {
             for (int64_t i = 0; i < n_slots; ++i) {

@@ -55,7 +55,7 @@ struct PathJump {
                     wr = __shfl(w, r);
                 p = slots[(wr << D) + j];
             }
-            const float xv = tile[r * RS + (p.f ^ dev::swz<RS>(r))];
+            const float xv = dev::feature_at<kXF32, 1>(tile + r * RS, p, dev::swz<RS>(r));
             // node evaluation: the chosen child of slot j
             if (j > 0) path[j] = 2 * j + int(!(xv < p.t));
             dev::wave_sync();
