@@ -153,6 +153,20 @@ def test_special_values_ties_and_near_ties(dt, F):
     _check(dt, nodes, off, x, F, 6)
 
 
+@pytest.mark.parametrize("waves", [1, 3, 8, 12, 15, 16])
+def test_workgroup_shapes_and_chunkings(dt, waves):
+    """Other wavefront counts give other chunk budgets: one to many trees per LDS chunk,
+    walked in groups of four, three, two or one."""
+    w = W.config(5, n_samples=9000)
+    x = w.features()
+    want = oracle.forest_classes(w.nodes, w.tree_offsets, x, w.n_features, w.n_classes)
+    f = dt.Forest(w.nodes, w.tree_offsets, w.n_features, w.n_classes, waves_per_cu=waves)
+    xd = torch.from_numpy(x).cuda()
+    for algo in ALGOS:
+        got = f.classify(xd, algo=algo, out_kind="class_i32").cpu().numpy()
+        np.testing.assert_array_equal(got, want, err_msg=algo)
+
+
 @pytest.mark.parametrize("n", [1, 63, 65, 130, 1000, 70000])
 def test_ragged_sizes_and_strides(dt, n):
     w = W.config(5, n_samples=n)
