@@ -194,10 +194,12 @@ dt_status dt_encode_windows(const dt_node *nodes, int32_t n_nodes, int32_t n_fea
 dt_status dt_threshold_keys(const float *thresholds, int64_t n, dt_dtype type, uint16_t *keys);
 
 /*
- * Validate a tree, encode it for both decompositions and copy the encodings to the
- * current HIP device.  Synchronous: the upload is complete on return.  The caller keeps
- * ownership of `nodes`.  The handle owns its device memory and is bound to the device
- * that was current at creation.
+ * Upload a tree (Section 3.1: the breadth-first node array of Procedure 1, evaluated by
+ * the recursive descent of Section 2.1; Section 3.3: the decision nodes the speculative
+ * decomposition maps to lanes).  Validate it, encode it for both decompositions and copy
+ * the encodings to the current HIP device.  Synchronous: the upload is complete on
+ * return.  The caller keeps ownership of `nodes`.  The handle owns its device memory and
+ * is bound to the device that was current at creation.
  * Errors: as dt_tree_check, DT_ERR_HIP, DT_ERR_NO_MEMORY.  *out is set only on DT_OK.
  */
 dt_status dt_tree_create(const dt_node *nodes, int32_t n_nodes, int32_t n_features,
@@ -230,7 +232,10 @@ dt_status dt_tree_launch_info(const dt_tree *tree, const void *d_x, dt_dtype x_t
                               dt_launch_info *info);
 
 /*
- * Classify n records.  Asynchronous on `stream` (a hipStream_t; NULL = the null stream).
+ * Classify n records: the label of the leaf each record reaches from the root, taking the
+ * left child when x[feature] < threshold (Section 2.1's evaluation; Section 3.2,
+ * Procedure 3 for DT_ALGO_DATA; Sections 3.3-3.4, Procedures 4-5 for DT_ALGO_SPECULATIVE
+ * and DT_ALGO_PATH).  Asynchronous on `stream` (a hipStream_t; NULL = the null stream).
  *   d_x     device pointer, row-major fp32, record r at d_x + r*ld, columns
  *           0..n_features-1 are read.  Any alignment of 4 bytes; rows that are
  *           contiguous (ld == n_features), a multiple of 4 floats and 16-byte aligned
@@ -238,7 +243,8 @@ dt_status dt_tree_launch_info(const dt_tree *tree, const void *d_x, dt_dtype x_t
  *   n       number of records, >= 0 (0: nothing is launched)
  *   ld      row stride in floats, >= n_features
  *   d_out   device pointer to n labels of the type named by out_kind
- *   algo    DT_ALGO_DATA or DT_ALGO_SPECULATIVE; both give identical results
+ *   algo    DT_ALGO_DATA, DT_ALGO_SPECULATIVE or DT_ALGO_PATH; all give identical
+ *           results
  * Exactly n outputs are written; nothing is written on an error return.  Buffers are
  * owned by the caller and must stay valid until the work on `stream` completes.
  * Errors: DT_ERR_INVALID_ARG (null tree or pointers with n > 0, n < 0, ld < n_features,
@@ -251,7 +257,8 @@ dt_status dt_classify(const dt_tree *tree, const float *d_x, int64_t n, int64_t 
                       void *d_out, dt_output out_kind, dt_algo algo, void *stream);
 
 /*
- * dt_classify for records of element type x_type (dt_dtype): d_x must be aligned to the
+ * dt_classify for narrow records (Section 2.1: ordered discrete attributes behave like the
+ * real-valued ones).  Records of element type x_type (dt_dtype): d_x must be aligned to the
  * element size and ld counts elements.  Rows that are contiguous, 16-byte aligned and a
  * multiple of 16 bytes long take the vectorised load path.  Each element is widened
  * exactly to fp32 before its comparison, so the labels equal those of dt_classify on the
@@ -263,7 +270,9 @@ dt_status dt_classify_typed(const dt_tree *tree, const void *d_x, dt_dtype x_typ
                             void *stream);
 
 /*
- * Forest of n_trees trees: tree k occupies nodes[tree_offsets[k] .. tree_offsets[k+1])
+ * Upload a forest: several trees evaluated one after another and combined (Section 1,
+ * the concatenated-trees scheme it cites), each tree in the layout of Procedure 1
+ * (Section 3.1).  Tree k occupies nodes[tree_offsets[k] .. tree_offsets[k+1])
  * with child indices local to that range (each tree is a valid array on its own).
  * tree_offsets has n_trees + 1 entries, starts at 0 and increases strictly.  All trees
  * share n_features and n_classes.  Synchronous upload, as dt_tree_create.
@@ -278,7 +287,8 @@ dt_status dt_forest_create(const dt_node *nodes, const int32_t *tree_offsets,
 void dt_forest_destroy(dt_forest *forest);
 
 /*
- * Majority vote of the forest's trees for n records; ties go to the smallest class id.
+ * Majority vote of the forest's trees for n records; ties go to the smallest class id
+ * (Section 1's forests; each tree evaluated as dt_classify, Sections 3.2-3.4).
  * Arguments and errors as dt_classify; out_kind must be DT_OUT_CLASS_U8 or
  * DT_OUT_CLASS_I32.
  */
@@ -324,7 +334,9 @@ typedef struct {
 } dt_pipeline_stats;
 
 /*
- * Pipeline for records of n_features floats, on the current device.  Allocates its device
+ * Pipeline for records of n_features floats, on the current device (Section 4.3's remedy
+ * for copy-dominated outer time: pinned host buffers and copies overlapped with the
+ * kernels).  Allocates its device
  * and pinned host buffers and creates its streams (default priority) here, never in a
  * call (unless `serial`).  opt may be NULL.
  * Errors: DT_ERR_INVALID_ARG (null out, n_features not 1..256, option out of range),
@@ -333,11 +345,13 @@ typedef struct {
 dt_status dt_pipeline_create(int32_t n_features, const dt_pipeline_options *opt,
                              dt_pipeline **out);
 
-/* Free a pipeline (waits for its streams first).  NULL is a no-op. */
+/* Free a pipeline (Section 4.3's overlapped copies; waits for its streams first).  NULL is
+ * a no-op. */
 void dt_pipeline_destroy(dt_pipeline *pipeline);
 
 /*
- * Labels of n host-resident records (h_x: n rows of the tree's n_features floats, row
+ * Outer-time classification (Section 4.2: the whole call, copies included, as Table 1's
+ * outer times measure it).  Labels of n host-resident records (h_x: n rows of the tree's n_features floats, row
  * stride ld >= n_features floats) written to the host buffer h_out (n uint8 or int32
  * values).  Synchronous: returns when h_out is complete; the buffers are only read and
  * written during the call.  Page-locked buffers (allocated with hipHostMalloc, or
@@ -352,14 +366,17 @@ dt_status dt_classify_host(const dt_tree *tree, dt_pipeline *pipeline, const flo
                            int64_t n, int64_t ld, void *h_out, dt_output out_kind,
                            dt_algo algo, dt_pipeline_stats *stats);
 
-/* As dt_classify_host for records of element type x_type (dt_classify_typed): h_x holds
+/* Outer-time classification (Section 4.2) of narrow records (Section 2.1's ordered
+ * discrete attributes).  As dt_classify_host for records of element type x_type
+ * (dt_classify_typed): h_x holds
  * elements of x_type (aligned to the element size), ld counts elements.  Narrow records
  * cross PCIe in their own width.  Errors: as dt_classify_host and dt_classify_typed. */
 dt_status dt_classify_host_typed(const dt_tree *tree, dt_pipeline *pipeline, const void *h_x,
                                  dt_dtype x_type, int64_t n, int64_t ld, void *h_out,
                                  dt_output out_kind, dt_algo algo, dt_pipeline_stats *stats);
 
-/* As dt_classify_host for a forest's majority vote (dt_forest_classify). */
+/* Outer-time classification (Section 4.2) of a forest's majority vote (Section 1): as
+ * dt_classify_host for dt_forest_classify. */
 dt_status dt_forest_classify_host(const dt_forest *forest, dt_pipeline *pipeline,
                                   const float *h_x, int64_t n, int64_t ld, void *h_out,
                                   dt_output out_kind, dt_algo algo, dt_pipeline_stats *stats);

@@ -107,6 +107,36 @@ def test_config4_full_size(dt):
         np.testing.assert_array_equal(got.cpu().numpy(), want_leaf, err_msg=algo)
 
 
+@pytest.mark.parametrize("sd", [3, 4, 5, 6])
+def test_config4_tree_every_wide_spec_window_depth(dt, sd):
+    """The C4 tree (complete depth 12, 4,095 decision nodes) with the wide speculative
+    windows: at depth 6 it is cut into 1 + 64 full 63-slot windows (subtree blocking,
+    Section 3.4 and the windows of Section 6).  200,000 seeded rows of the C4 records with
+    exact ties planted on every path level and NaN features."""
+    w = W.config(4, n_samples=200_000)
+    x = w.features()
+    F = w.n_features
+    r = np.random.Generator(np.random.PCG64(4000 + sd))
+    # ties: set the feature a row tests at some level of its own path to that threshold
+    leaf = oracle.tree_leaves(w.nodes, x, F)
+    rows = r.choice(x.shape[0], size=20_000, replace=False)
+    for s in rows:
+        i = 0
+        level = int(r.integers(0, 12))
+        for _ in range(level):
+            i = w.nodes["left"][i] + int(not (x[s, w.nodes["feature"][i]] < w.nodes["threshold"][i]))
+        x[s, w.nodes["feature"][i]] = w.nodes["threshold"][i]
+    nan_rows = r.choice(x.shape[0], size=5_000, replace=False)
+    x[nan_rows, r.integers(0, F, size=nan_rows.size)] = np.nan
+    x[::4099, :] = np.nan
+    assert (oracle.tree_leaves(w.nodes, x, F) != leaf).any()     # the planting moved rows
+    t = dt.Tree(w.nodes, F, w.n_classes, spec_window_depth=sd)
+    info = t.info
+    print("C4 tree, spec depth", sd, info, flush=True)
+    assert info["spec_window_depth"] == sd
+    _check_all_outputs(dt, t, w.nodes, x, _gpu(x), F)
+
+
 @pytest.mark.parametrize("hops", [1, 2, 3, 8])
 @pytest.mark.parametrize("sd", [1, 3, 4, 6])
 def test_path_reduction_hops(dt, hops, sd):

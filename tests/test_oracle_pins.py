@@ -377,3 +377,68 @@ def test_sweep_rows():
     np.testing.assert_array_equal(np.sort(xs, axis=0), np.sort(xi, axis=0))
     # neighbouring pixels of the coherent raster are close, the i.i.d. records are not
     assert np.abs(np.diff(xc, axis=0)).mean() < 0.1 < 0.3 < np.abs(np.diff(xi, axis=0)).mean()
+
+
+# ------------------------------------------------------- threaded row-chunk wrapper
+
+def _python_walk(nodes, x):
+    """Leaf of every row by the plain root-to-leaf walk (Section 2.1's evaluation), one
+    row at a time in Python: independent of the C oracle and of its row chunking."""
+    out = np.empty(x.shape[0], dtype=np.int32)
+    for s in range(x.shape[0]):
+        i = 0
+        while nodes["cls"][i] < 0:
+            i = nodes["left"][i] if x[s, nodes["feature"][i]] < nodes["threshold"][i] \
+                else nodes["left"][i] + 1
+        out[s] = i
+    return out
+
+
+@pytest.mark.parametrize("threads", [2, 3, 16])
+@pytest.mark.parametrize("n", [0, 1, 2, 5, 17, 1001])
+def test_threaded_wrapper_equals_serial_call(threads, n):
+    """The oracle split over contiguous row chunks on several host threads returns the
+    serial call's result for every row: uneven splits (n not a multiple of the thread
+    count), more threads than rows, no rows, a one-row matrix, and rows with ld > F."""
+    r = rng(9100 + 31 * threads + n)
+    F = 6
+    nodes = W.random_full_tree(r, 40, F, 5)
+    wide = W.uniform_f32(r, (n, F + 3))
+    forest_trees = [W.random_full_tree(r, int(r.integers(1, 30)), F, 5) for _ in range(7)]
+    fnodes, foff = _forest(forest_trees)
+    for x in (np.ascontiguousarray(wide[:, :F]), wide[:, :F]):      # ld == F, ld == F + 3
+        if n > 1:
+            assert x.strides[0] // 4 in (F, F + 3)
+        leaves = oracle.tree_leaves(nodes, x, F, threads=threads)
+        np.testing.assert_array_equal(leaves, oracle.tree_leaves(nodes, x, F))
+        np.testing.assert_array_equal(leaves, _python_walk(nodes, x))
+        np.testing.assert_array_equal(oracle.tree_classes(nodes, x, F, threads=threads),
+                                      nodes["cls"][_python_walk(nodes, x)])
+        np.testing.assert_array_equal(
+            oracle.forest_classes(fnodes, foff, x, F, 5, threads=threads),
+            oracle.forest_classes(fnodes, foff, x, F, 5))
+
+
+def test_threaded_wrapper_row_chunks_cover_every_row_once():
+    """Each row is written by exactly one chunk: a row whose features send it to a
+    distinct leaf per position shows up in the right place at every thread count."""
+    F = 1
+    depth = 7
+    t = np.arange(1, 1 << depth, dtype=np.float32)           # thresholds 1 .. 127
+    nodes = np.zeros(2 * len(t) + 1, dtype=W.NODE_DTYPE)
+    counter = {"t": 0, "leaf": 0}
+
+    def inorder(h, d):
+        if d == depth:
+            nodes[h] = (0, 0.0, -1, counter["leaf"]); counter["leaf"] += 1
+            return
+        inorder(2 * h + 1, d + 1)
+        nodes[h] = (0, t[counter["t"]], 2 * h + 1, -1); counter["t"] += 1
+        inorder(2 * h + 2, d + 1)
+
+    inorder(0, 0)
+    for n in (1, 7, 100, 128):
+        x = (np.arange(n, dtype=np.float32) % 128)[:, None]
+        for threads in (1, 2, 3, 16, 200):
+            got = oracle.tree_classes(nodes, x, F, threads=threads)
+            np.testing.assert_array_equal(got, np.arange(n) % 128)
