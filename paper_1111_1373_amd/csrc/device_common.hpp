@@ -323,6 +323,15 @@ __device__ __forceinline__ void stage_now(const Rows &in, float *tile, int64_t t
     }
 }
 
+// v_writelane_b32: `value` (wavefront-uniform) written into lane `lane` of `old`.  The
+// compiler's intrinsic has no clang builtin here, so it is declared by its LLVM name.
+extern "C" __device__ int dt_llvm_writelane(int value, int lane, int old)
+    __asm("llvm.amdgcn.writelane.i32");
+
+__device__ __forceinline__ uint32_t writelane(uint32_t value, int lane, uint32_t old) {
+    return uint32_t(dt_llvm_writelane(int(value), lane, int(old)));
+}
+
 // One heap step, p <- 2p + b, as a single add with carry: the compare that produces b
 // leaves it as a wave mask in scalar registers, which v_addc takes as its carry-in, so
 // the step costs one vector instruction instead of a select and a shift-or.  Lanes
@@ -446,86 +455,97 @@ struct Spec {
     __device__ __forceinline__ explicit Spec(int lane)
         : j(lane & (S - 1)), seg_shift(lane & ~(S - 1)) {}
 
-    // Segments of 2, 4 or 16 lanes broadcast a lane's value to its segment with one DPP
-    // move (quad_perm within groups of 4 lanes, row_share within rows of 16); the round
-    // index must then be a compile-time constant.
-    static constexpr bool kDpp = S == 2 || S == 4 || S == 16;
-
-    // Value w of lane seg_shift + G (record seg_shift + G's window offset) in every lane of
-    // the segment.  Every source lane is in range and enabled, so no old value is needed.
+    // Value wb of lane seg_shift + G (record seg_shift + G's window byte offset) in every
+    // lane of the segment, with the round index G a compile-time constant:
+    //   2, 4, 16 lanes: one DPP move (quad_perm within groups of 4 lanes, row_share within
+    //     rows of 16), which folds into the slot address add;
+    //   8, 32 lanes: ds_swizzle in bitmask mode (within each half-wave, lane i reads lane
+    //     (i & and_mask) | G): no address computation, no VALU instruction;
+    //   64 lanes: readlane into a scalar register.
+    // Every source lane is in range and enabled, so no old value is needed.
     template <int G>
-    __device__ __forceinline__ int window_of(int w) const {
-        if constexpr (S == 16)
-            return __builtin_amdgcn_mov_dpp(w, 0x150 + G, 0xF, 0xF, true);   // row_share
+    __device__ __forceinline__ int window_of(int wb) const {
+        if constexpr (S == 64)
+            return __builtin_amdgcn_readlane(wb, G);
+        else if constexpr (S == 32)
+            return __builtin_amdgcn_ds_swizzle(wb, G << 5);          // and 0, or G
+        else if constexpr (S == 16)
+            return __builtin_amdgcn_mov_dpp(wb, 0x150 + G, 0xF, 0xF, true);   // row_share
+        else if constexpr (S == 8)
+            return __builtin_amdgcn_ds_swizzle(wb, G << 5 | 0x18);   // and 0b11000, or G
         else if constexpr (S == 4)
-            return __builtin_amdgcn_mov_dpp(w, G * 0x55, 0xF, 0xF, true);    // quad_perm
+            return __builtin_amdgcn_mov_dpp(wb, G * 0x55, 0xF, 0xF, true);    // quad_perm
         else   // S == 2: quad_perm [G, G, 2 + G, 2 + G]
-            return __builtin_amdgcn_mov_dpp(w, G | G << 2 | (2 + G) << 4 | (2 + G) << 6,
+            return __builtin_amdgcn_mov_dpp(wb, G | G << 2 | (2 + G) << 4 | (2 + G) << 6,
                                             0xF, 0xF, true);
     }
 
-    // Round g: the segment starting at lane b evaluates record b + g, so record r's bits
-    // arrive in r's own segment in the round g == r % S.
-    __device__ __forceinline__ void round(int g, int wb, Bits &bits, const Slot *slots, bool first,
-                                          const Slot &root, const T *tile) const {
-        const int r = seg_shift + g;
-        // wb: byte offset of record r's window, window id * 2^D * sizeof(Slot); adding it to
-        // this lane's own slot address folds into the broadcast (one DPP add per round)
-        const Slot p = first ? root
-                             : *reinterpret_cast<const Slot *>(
-                                   reinterpret_cast<const char *>(slots + j) + wb);
-        const T xv = feature_at<XT, 1>(tile + r * RS, p, swz_el<XT, RS>(r));
-        const uint64_t m = __ballot(N::right(xv, p));
-        if (j == g) bits = Bits(m >> seg_shift);
+    // Round G's mask m (bit i: slot i - seg_shift of record seg_shift + G, for the lanes i
+    // of each segment) goes to lane seg_shift + G as that record's bits.  Segments of 32 and
+    // 64 lanes write the scalar mask straight into the lane (v_writelane: one instruction
+    // per 32 bits); narrower ones shift the mask by the segment and select the lane.
+    template <int G>
+    __device__ __forceinline__ void take(Bits &bits, uint64_t m) const {
+        if constexpr (S == 64) {
+            const uint32_t lo = writelane(uint32_t(m), G, uint32_t(bits));
+            const uint32_t hi = writelane(uint32_t(m >> 32), G, uint32_t(bits >> 32));
+            bits = uint64_t(hi) << 32 | lo;
+        } else if constexpr (S == 32) {
+            bits = writelane(uint32_t(m), G, bits);
+            bits = writelane(uint32_t(m >> 32), 32 + G, bits);
+        } else {
+            if (j == G) bits = Bits(m >> seg_shift);
+        }
     }
 
-    // Rounds G0 + G... (a group of 4 or 8: a scheduling barrier after each group keeps the
-    // compiler from holding every round's loads in registers at once).
+    // Rounds G0 + G... as one batch: the slot reads of every round are issued, then the
+    // feature reads, then the compares, so a batch waits for two LDS round trips rather
+    // than two per round.  In round g the segment starting at lane b evaluates record
+    // b + g, so record r's bits arrive in r's own lane in the round g == r % S.  A
+    // scheduling barrier after each batch keeps the compiler from holding every round's
+    // loads in registers at once.
     template <int G0, int... G>
-    __device__ __forceinline__ void eval_dpp(std::integer_sequence<int, G...>, Bits &bits,
-                                             const Slot *slots, bool first, const Slot &root,
-                                             int w, const T *tile) const {
-        (round(G0 + G, first ? 0 : window_of<G0 + G>(w * int(sizeof(Slot) << D)), bits, slots,
-               first, root, tile), ...);
+    __device__ __forceinline__ void eval_batch(std::integer_sequence<int, G...>, Bits &bits,
+                                               const Slot *slots, bool first, const Slot &root,
+                                               int wb, const T *tile) const {
+        constexpr int K = sizeof...(G);
+        Slot p[K];
+        // wb: byte offset of the record's window, window id * 2^D * sizeof(Slot); added to
+        // this lane's own slot address
+        ((p[G] = first ? root
+                       : *reinterpret_cast<const Slot *>(
+                             reinterpret_cast<const char *>(slots + j) + window_of<G0 + G>(wb))),
+         ...);
+        T xv[K];
+        ((xv[G] = feature_at<XT, 1>(tile + (seg_shift + G0 + G) * RS, p[G],
+                                    swz_el<XT, RS>(seg_shift + G0 + G))),
+         ...);
+        (take<G0 + G>(bits, __ballot(N::right(xv[G], p[G]))), ...);
         __builtin_amdgcn_sched_barrier(0);
     }
 
     template <int K, int... Q>
-    __device__ __forceinline__ void eval_groups(std::integer_sequence<int, Q...>,
-                                                std::integral_constant<int, K>, Bits &bits,
-                                                const Slot *slots, bool first, const Slot &root,
-                                                int w, const T *tile) const {
-        (eval_dpp<Q * K>(std::make_integer_sequence<int, K>(), bits, slots, first, root, w, tile),
+    __device__ __forceinline__ void eval_batches(std::integer_sequence<int, Q...>,
+                                                 std::integral_constant<int, K>, Bits &bits,
+                                                 const Slot *slots, bool first, const Slot &root,
+                                                 int wb, const T *tile) const {
+        (eval_batch<Q * K>(std::make_integer_sequence<int, K>(), bits, slots, first, root, wb,
+                           tile),
          ...);
     }
+
+    // Rounds per batch: 8, or 4 where wide record tiles keep a 64-register prefetch
+    // buffer live next to groups of up to 16 lanes.
+    static constexpr int kBatch = S < 8 ? S : (RS >= 64 && S <= 16 ? 4 : 8);
 
     // One window level for the 64 records.
     __device__ __forceinline__ Bits eval(const Slot *slots, bool first, const Slot &root, int w,
                                          const T *tile) const {
-        if constexpr (kDpp) {
-            // wide tiles keep a 64-register prefetch buffer live: smaller groups there
-            constexpr int kMaxGroup = RS >= 64 ? 4 : 8;
-            constexpr int kGroup = S < kMaxGroup ? S : kMaxGroup;
-            Bits bits = 0;
-            eval_groups(std::make_integer_sequence<int, S / kGroup>(),
-                        std::integral_constant<int, kGroup>(), bits, slots, first, root, w, tile);
-            return bits;
-        } else {
-            Bits bits = 0;
-#pragma unroll 8
-            for (int g = 0; g < S; ++g) {
-                int wr = 0;
-                if (!first) {
-                    const int wb = w * int(sizeof(Slot) << D);
-                    if constexpr (S == 64)
-                        wr = __builtin_amdgcn_readlane(wb, g);
-                    else
-                        wr = __shfl(wb, seg_shift + g);
-                }
-                round(g, wr, bits, slots, first, root, tile);
-            }
-            return bits;
-        }
+        Bits bits = 0;
+        eval_batches(std::make_integer_sequence<int, S / kBatch>(),
+                     std::integral_constant<int, kBatch>(), bits, slots, first, root,
+                     first ? 0 : w * int(sizeof(Slot) << D), tile);
+        return bits;
     }
 
     // Exit index reached from the window root (slot 1) by following the bits: p <- 2p + b_p.
