@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define DT_ABI_VERSION 4
+#define DT_ABI_VERSION 5
 
 typedef enum {
     DT_OK = 0,
@@ -217,10 +217,13 @@ typedef struct {
     int32_t waves_per_workgroup;
     int32_t workgroups_per_cu;     /* resident workgroups per compute unit               */
     int32_t lds_bytes;             /* dynamic LDS per workgroup                          */
-    int32_t result_buffer_tiles;   /* tiles of 64 results each wavefront buffers        */
+    int32_t result_buffer_tiles;   /* tiles of results each wavefront buffers           */
     int32_t tables_in_lds;         /* 1: tree tables staged in the LDS, 0: read in place */
     int32_t load_mode;             /* 0: scalar loads, 1: 16-byte loads, 2: 16-byte loads
                                       of rows exactly one LDS row stride wide            */
+    int32_t tile_rows;             /* records per wavefront tile: 64, or 32 for the
+                                      speculative walk of 64-slot windows on rows of at
+                                      least 32 bytes                                     */
 } dt_launch_info;
 
 /* Fill *info with the launch shape of dt_classify_typed(tree, d_x, x_type, n, ld, ...,

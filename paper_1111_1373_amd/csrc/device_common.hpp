@@ -149,25 +149,34 @@ __device__ __forceinline__ uint32_t div_w(uint32_t e, const Rows &in) {
     return in.n_words == 1 ? e : __umulhi(e, in.magic_w);
 }
 
+// Records of tile `tile` (tiles of TR records) that exist in the input.
+template <int TR = kTileRows>
 __device__ __forceinline__ int valid_rows(const Rows &in, int64_t tile) {
-    const int64_t left = in.n - tile * kTileRows;
-    return left < kTileRows ? int(left) : kTileRows;
+    const int64_t left = in.n - tile * TR;
+    return left < TR ? int(left) : TR;
 }
 
 // Tile layouts.  Row-major (the default): row r at word r*RSW, word w at w ^ swz(r).
 // Column-major (fp32 only, used where every lane reads its own record): column c at word
 // c*64, row r at c*64 + r, so lane r always reads bank r, whatever column it asks for.
-enum TileLayout { kRowMajor = 0, kColMajor = 1 };
+// Flat row-major: row r at word r*RSW, word w at w, for kernels whose wavefront reads one
+// row at a time (64-lane record groups): a single row is conflict-free without the
+// swizzle, and staging then stores whole 16-byte vectors.
+enum TileLayout { kRowMajor = 0, kColMajor = 1, kRowFlat = 2 };
 
 // Store 4 consecutive words (c % 4 == 0) of row r into the tile (rows of RSW words;
 // `tile` is the word view of the tile).
 template <int RSW, int LAYOUT = kRowMajor>
 __device__ __forceinline__ void put4(float *tile, int r, int c, f32x4 v) {
-    if constexpr (LAYOUT == kColMajor) {
+    if constexpr (LAYOUT == kColMajor) {   // 64-record tiles only
         tile[(c + 0) * kTileRows + r] = v.x;
         tile[(c + 1) * kTileRows + r] = v.y;
         tile[(c + 2) * kTileRows + r] = v.z;
         tile[(c + 3) * kTileRows + r] = v.w;
+        return;
+    }
+    if constexpr (LAYOUT == kRowFlat) {
+        *reinterpret_cast<f32x4 *>(tile + r * RSW + c) = v;
         return;
     }
     float *row = tile + r * RSW;
@@ -179,9 +188,9 @@ __device__ __forceinline__ void put4(float *tile, int r, int c, f32x4 v) {
 }
 
 // Vectorised staging (dense rows of n_words 4-byte words, n_words % 4 == 0, 16-byte
-// aligned base), one tile held in registers so that the next tile's loads overlap the walk
-// of the current one.  RSW = LDS row stride in words.  The element type does not matter
-// here: words are moved unchanged.
+// aligned base), one tile of TR records held in registers so that the next tile's loads
+// overlap the walk of the current one.  RSW = LDS row stride in words.  The element type
+// does not matter here: words are moved unchanged.
 //
 // Loads are never guarded by a branch: guarded loads compile into branches whose joins
 // copy the loaded registers, which forces a wait for every outstanding load right after
@@ -189,15 +198,15 @@ __device__ __forceinline__ void put4(float *tile, int r, int c, f32x4 v) {
 // the last valid vector instead, so rows past the end of the input hold copies of valid
 // features; their results are never stored.  EXACT (n_words == RSW): every lane owns
 // RSW/4 vectors of a full tile and the LDS positions are shifts and masks.
-template <int RSW, bool EXACT>
+template <int RSW, bool EXACT, int TR = kTileRows>
 struct VecTile {
-    static constexpr int kVec = RSW / 4;   // 16-byte vectors per lane for n_words == RSW
-    static_assert(kVec >= 1, "vector staging needs rows of at least 16 bytes");
+    static constexpr int kVec = TR * RSW / 256;   // 16-byte vectors per lane for n_words == RSW
+    static_assert(kVec >= 1, "vector staging needs one 16-byte vector per lane and tile");
     f32x4 v[kVec];
 
     __device__ __forceinline__ const f32x4 *base(const Rows &in, int64_t tile) const {
         return reinterpret_cast<const f32x4 *>(static_cast<const char *>(in.x) +
-                                               tile * kTileRows * in.n_words * 4);
+                                               tile * TR * in.n_words * 4);
     }
 
     // Any tile; nvec = vectors holding valid records (>= 1).
@@ -217,13 +226,13 @@ struct VecTile {
 #pragma unroll
             for (int k = 0; k < kVec; ++k) v[k] = __builtin_nontemporal_load(src + k * 64);
         } else {
-            load_clamped(in, tile, lane, kTileRows * in.n_words / 4);
+            load_clamped(in, tile, lane, TR * in.n_words / 4);
         }
     }
 
     // Any tile, including the partial last one.
     __device__ __forceinline__ void load_tail(const Rows &in, int64_t tile, int lane) {
-        load_clamped(in, tile, lane, (valid_rows(in, tile) * in.n_words) >> 2);
+        load_clamped(in, tile, lane, (valid_rows<TR>(in, tile) * in.n_words) >> 2);
     }
 
     template <int LAYOUT = kRowMajor>
@@ -236,7 +245,7 @@ struct VecTile {
                 put4<RSW, LAYOUT>(tile, e >> sh, e & (RSW - 1), v[k]);
             }
         } else {
-            const int full = kTileRows * in.n_words / 4;
+            const int full = TR * in.n_words / 4;
 #pragma unroll
             for (int k = 0; k < kVec; ++k) {
                 const int q = k * 64 + lane;
@@ -252,14 +261,14 @@ struct VecTile {
 
 // Vectorised staging of wide rows (RSW > 64 words) in chunks of 16 vectors per lane,
 // without prefetch (loads clamped to the valid vectors as in VecTile).
-template <int RSW, int LAYOUT = kRowMajor>
+template <int RSW, int LAYOUT = kRowMajor, int TR = kTileRows>
 __device__ __forceinline__ void stage_wide(const Rows &in, float *tile, int64_t t, int lane) {
-    const int nvec = (valid_rows(in, t) * in.n_words) >> 2;
-    const int full = kTileRows * in.n_words / 4;
+    const int nvec = (valid_rows<TR>(in, t) * in.n_words) >> 2;
+    const int full = TR * in.n_words / 4;
     const f32x4 *src = reinterpret_cast<const f32x4 *>(static_cast<const char *>(in.x) +
-                                                       t * kTileRows * in.n_words * 4);
+                                                       t * TR * in.n_words * 4);
 #pragma unroll 1
-    for (int k0 = 0; k0 < RSW / 4; k0 += 16) {
+    for (int k0 = 0; k0 < TR * RSW / 256; k0 += 16) {
         f32x4 v[16];
 #pragma unroll
         for (int k = 0; k < 16; ++k) {
@@ -279,23 +288,28 @@ __device__ __forceinline__ void stage_wide(const Rows &in, float *tile, int64_t 
 }
 
 // General staging: any ld >= F, element-aligned, one element per load.
-template <int XT, int RS, int LAYOUT = kRowMajor>
+template <int XT, int RS, int LAYOUT = kRowMajor, int TR = kTileRows>
 __device__ __forceinline__ void stage_scalar(const Rows &in, float *tile_words, int64_t t,
                                              int lane) {
-    static_assert(LAYOUT == kRowMajor || XT == kXF32, "column-major tiles hold fp32 records");
+    static_assert(LAYOUT != kColMajor || XT == kXF32, "column-major tiles hold fp32 records");
     using T = typename Elem<XT>::T;
     T *tile = reinterpret_cast<T *>(tile_words);
     const T *x = static_cast<const T *>(in.x);
-    const int64_t row0 = t * kTileRows;
-    const int valid = valid_rows(in, t);
-    for (int k = 0; k < in.n_features; ++k) {
+    static_assert(LAYOUT != kColMajor || TR == kTileRows, "column-major tiles hold 64 records");
+    const int64_t row0 = t * TR;
+    const int valid = valid_rows<TR>(in, t);
+    // TR * F elements, 64 per pass (TR is 32 or 64)
+    for (int k = 0; k < (TR == kTileRows ? in.n_features : (in.n_features + 1) >> 1); ++k) {
         const uint32_t idx = uint32_t(k * 64 + lane);
         const int r = int(div_f(idx, in));
         const int c = int(idx) - r * in.n_features;
+        if (r >= TR) break;            // only in the last pass of a 32-record tile, odd F
         T v = T(0);
         if (r < valid) v = x[(row0 + r) * in.ld + c];
         if constexpr (LAYOUT == kColMajor)
             tile[c * kTileRows + r] = v;
+        else if constexpr (LAYOUT == kRowFlat)
+            tile[r * RS + c] = v;
         else
             tile[r * RS + (c ^ swz_el<XT, RS>(r))] = v;
     }
@@ -305,21 +319,21 @@ __device__ __forceinline__ void stage_scalar(const Rows &in, float *tile_words, 
 // path (16-byte loads, at least one vector per lane and row) exists for it.
 template <int XT, int RS>
 constexpr int row_words() { return RS * int(sizeof(typename Elem<XT>::T)) / 4; }
-template <int XT, int RS>
-constexpr bool has_vec_staging() { return row_words<XT, RS>() >= 4; }
+template <int XT, int RS, int TR = kTileRows>
+constexpr bool has_vec_staging() { return TR * row_words<XT, RS>() >= 256; }
 
-// Stage tile t without register prefetch.
-template <int XT, int RS, int LOAD, int LAYOUT = kRowMajor>
+// Stage tile t (of TR records) without register prefetch.
+template <int XT, int RS, int LOAD, int LAYOUT = kRowMajor, int TR = kTileRows>
 __device__ __forceinline__ void stage_now(const Rows &in, float *tile, int64_t t, int lane) {
     constexpr int RSW = row_words<XT, RS>();
-    if constexpr (LOAD != kLoadScalar && has_vec_staging<XT, RS>() && RSW <= 64) {
-        VecTile<RSW, LOAD == kLoadExact> buf;
+    if constexpr (LOAD != kLoadScalar && has_vec_staging<XT, RS, TR>() && RSW <= 64) {
+        VecTile<RSW, LOAD == kLoadExact, TR> buf;
         buf.load_tail(in, t, lane);
         buf.template store<LAYOUT>(in, tile, lane);
-    } else if constexpr (LOAD != kLoadScalar && has_vec_staging<XT, RS>()) {
-        stage_wide<RSW, LAYOUT>(in, tile, t, lane);
+    } else if constexpr (LOAD != kLoadScalar && has_vec_staging<XT, RS, TR>()) {
+        stage_wide<RSW, LAYOUT, TR>(in, tile, t, lane);
     } else {
-        stage_scalar<XT, RS, LAYOUT>(in, tile, t, lane);
+        stage_scalar<XT, RS, LAYOUT, TR>(in, tile, t, lane);
     }
 }
 
@@ -442,15 +456,24 @@ __device__ __forceinline__ void walk_data_k(const char *const (&base)[K], const 
 // wavefront instruction evaluates 64/S records' windows.  One ballot gathers the 64
 // outcomes; record r's segment is handed to lane r, which walks its bits from the window
 // root to the exit.
-template <int XT, int RS, int D>
+template <int XT, int RS, int D, int TR = kTileRows>
 struct Spec {
     using T = typename Elem<XT>::T;
     using N = Node<XT>;
     using Slot = typename N::S;
     static constexpr int S = 1 << D;
+    // Tiles of TR records: 64, or 32 for 64-lane groups (one record per round, so a round
+    // count of TR covers the tile; lanes >= TR carry no record).
+    static_assert(TR == kTileRows || (S == 64 && TR == 32), "32-record tiles need 64-lane groups");
+    static constexpr int kRounds = S == 64 ? TR : S;
     using Bits = typename std::conditional<(S > 32), uint64_t, uint32_t>::type;
     int j;          // slot evaluated by this lane (slot 0 is padding)
     int seg_shift;  // first lane of this lane's segment
+
+    // Record tile layout the rounds read: a 64-lane group reads one record row per round
+    // (conflict-free without the swizzle, flat rows); narrower groups read 64/S rows at
+    // once, and the swizzle keeps rows reading the same feature on distinct banks.
+    static constexpr int kLayout = S == 64 ? kRowFlat : kRowMajor;
 
     __device__ __forceinline__ explicit Spec(int lane)
         : j(lane & (S - 1)), seg_shift(lane & ~(S - 1)) {}
@@ -518,7 +541,7 @@ struct Spec {
          ...);
         T xv[K];
         ((xv[G] = feature_at<XT, 1>(tile + (seg_shift + G0 + G) * RS, p[G],
-                                    swz_el<XT, RS>(seg_shift + G0 + G))),
+                                    kLayout == kRowFlat ? 0 : swz_el<XT, RS>(seg_shift + G0 + G))),
          ...);
         (take<G0 + G>(bits, __ballot(N::right(xv[G], p[G]))), ...);
         __builtin_amdgcn_sched_barrier(0);
@@ -534,15 +557,19 @@ struct Spec {
          ...);
     }
 
-    // Rounds per batch: 8, or 4 where wide record tiles keep a 64-register prefetch
-    // buffer live next to groups of up to 16 lanes.
-    static constexpr int kBatch = S < 8 ? S : (RS >= 64 && S <= 16 ? 4 : 8);
+    // Rounds per batch: 8, or 4 where the tile's prefetch buffer takes 64 registers (16 KiB
+    // record tiles), which leaves too few for eight rounds' loads; never more than a level's
+    // rounds.
+    static constexpr int kPrefetchRegs = TR * RS * int(sizeof(T)) / 256;
+    static constexpr int kMaxBatch = kPrefetchRegs >= 64 ? 4 : 8;
+    static constexpr int kBatch = kRounds < kMaxBatch ? kRounds : kMaxBatch;
+    static_assert(kBatch >= 1 && kRounds % kBatch == 0, "batches must cover a level's rounds");
 
-    // One window level for the 64 records.
+    // One window level for the tile's records.
     __device__ __forceinline__ Bits eval(const Slot *slots, bool first, const Slot &root, int w,
                                          const T *tile) const {
         Bits bits = 0;
-        eval_batches(std::make_integer_sequence<int, S / kBatch>(),
+        eval_batches(std::make_integer_sequence<int, kRounds / kBatch>(),
                      std::integral_constant<int, kBatch>(), bits, slots, first, root,
                      first ? 0 : w * int(sizeof(Slot) << D), tile);
         return bits;
@@ -598,7 +625,7 @@ struct Spec {
         } else {
             int w = 0;
             int32_t code = exits[walk(eval(slots, true, root, 0, tile))];
-            bool done = code < 0;
+            bool done = code < 0 || (TR < kTileRows && j >= TR);   // lanes without a record
             if (!done) w = code;
             for (int level = 1; level < levels; ++level) {
                 if (__all(done)) break;
@@ -664,7 +691,7 @@ __device__ __forceinline__ void flush_results(const KArgs &a, const uint8_t *buf
     const int nbytes = int(r1 - r0) * esize;
     uint8_t *dst = static_cast<uint8_t *>(a.out) + r0 * esize;
     int done = 0;
-    if (a.out_vec) {   // dst is 16-byte aligned: r0 is a multiple of 64 records
+    if (a.out_vec) {   // dst is 16-byte aligned: r0 is a multiple of 32 or 64 records
         typedef int i32x4 __attribute__((ext_vector_type(4)));
         const int nvec = nbytes >> 4;
         for (int i = lane; i < nvec; i += 64)
@@ -680,12 +707,12 @@ __device__ __forceinline__ void flush_results(const KArgs &a, const uint8_t *buf
     }
 }
 
-// Persistent tile loop.  Wavefront g of G takes the contiguous tile range
-// [g*chunk, (g+1)*chunk), chunk = ceil(tiles / G), so its results form one contiguous run
-// of the output.  `body(t)` walks staged tile t and returns each lane's result.  No
-// workgroup barrier inside: the wavefronts of a workgroup process different numbers of
-// tiles.
-template <int XT, int RS, int LOAD, class Body>
+// Persistent tile loop over tiles of TR records.  Wavefront g of G takes the contiguous
+// tile range [g*chunk, (g+1)*chunk), chunk = ceil(tiles / G), so its results form one
+// contiguous run of the output.  `body(t)` walks staged tile t and returns each lane's
+// result (lane r: record r of the tile; lanes >= TR have none).  No workgroup barrier
+// inside: the wavefronts of a workgroup process different numbers of tiles.
+template <int XT, int RS, int LOAD, int LAYOUT = kRowMajor, int TR = kTileRows, class Body>
 __device__ __forceinline__ void tile_loop(const KArgs &a, float *tile, uint8_t *obuf, int lane,
                                           Body body) {
     constexpr int RSW = row_words<XT, RS>();
@@ -694,48 +721,50 @@ __device__ __forceinline__ void tile_loop(const KArgs &a, float *tile, uint8_t *
     const int64_t chunk = (a.in.n_tiles + G - 1) / G;
     const int64_t t0 = gw * chunk < a.in.n_tiles ? gw * chunk : a.in.n_tiles;
     const int64_t t1 = t0 + chunk < a.in.n_tiles ? t0 + chunk : a.in.n_tiles;
-    const int64_t n_full = a.in.n / kTileRows;     // tiles with 64 valid records
+    const int64_t n_full = a.in.n / TR;            // tiles with TR valid records
     const int esize = a.out_kind == 0 ? 1 : 4;
     int64_t fl = t0;                               // first tile whose results are buffered
 
     auto finish = [&](int64_t t, int32_t v) {
-        const int slot = int(t - fl) * kTileRows + lane;
-        if (esize == 1)
-            obuf[slot] = uint8_t(v);
-        else
-            reinterpret_cast<int32_t *>(obuf)[slot] = v;
+        const int slot = int(t - fl) * TR + lane;
+        if (TR == kTileRows || lane < TR) {
+            if (esize == 1)
+                obuf[slot] = uint8_t(v);
+            else
+                reinterpret_cast<int32_t *>(obuf)[slot] = v;
+        }
         if (t - fl == a.out_cap - 1 || t + 1 == t1) {
             wave_sync();
-            flush_results(a, obuf, fl * kTileRows, (t + 1) * kTileRows, lane);
+            flush_results(a, obuf, fl * TR, (t + 1) * TR, lane);
             wave_sync();
             fl = t + 1;
         }
     };
 
-    if constexpr (LOAD != kLoadScalar && has_vec_staging<XT, RS>() && RSW <= 64) {
+    if constexpr (LOAD != kLoadScalar && has_vec_staging<XT, RS, TR>() && RSW <= 64) {
         // Full tiles: the loads of tile t + 1 are in flight in registers while tile t is
         // walked.  The partial last tile of the input, if any, is staged on its own.
-        VecTile<RSW, LOAD == kLoadExact> buf;
+        VecTile<RSW, LOAD == kLoadExact, TR> buf;
         const int64_t tf = t1 < n_full ? t1 : n_full;
         int64_t t = t0;
         if (t < tf) buf.load_full(a.in, t, lane);
         for (; t < tf; ++t) {
             wave_sync();                 // previous tile fully read
-            buf.store(a.in, tile, lane);
+            buf.template store<LAYOUT>(a.in, tile, lane);
             wave_sync();                 // tile visible to every lane
             if (t + 1 < tf) buf.load_full(a.in, t + 1, lane);
             finish(t, body(t));
         }
         if (t < t1) {                         // t == n_full: the partial tile
             wave_sync();
-            stage_now<XT, RS, LOAD>(a.in, tile, t, lane);
+            stage_now<XT, RS, LOAD, LAYOUT, TR>(a.in, tile, t, lane);
             wave_sync();
             finish(t, body(t));
         }
     } else {
         for (int64_t t = t0; t < t1; ++t) {
             wave_sync();
-            stage_now<XT, RS, LOAD>(a.in, tile, t, lane);
+            stage_now<XT, RS, LOAD, LAYOUT, TR>(a.in, tile, t, lane);
             wave_sync();
             finish(t, body(t));
         }
@@ -743,14 +772,14 @@ __device__ __forceinline__ void tile_loop(const KArgs &a, float *tile, uint8_t *
 }
 
 // LDS layout: [tables (if staged)] [one record tile per wavefront] [one result buffer per
-// wavefront].  `tile` is the word view of this wavefront's tile.
-template <int XT, int RS>
+// wavefront].  `tile` is the word view of this wavefront's tile (TR records).
+template <int XT, int RS, int TR = kTileRows>
 __device__ __forceinline__ void wave_buffers(const KArgs &a, char *after_tables, float *&tile,
                                              uint8_t *&obuf) {
-    constexpr int kTileBytes = kTileRows * row_words<XT, RS>() * 4;
+    constexpr int kTileBytes = TR * row_words<XT, RS>() * 4;
     const int wave = threadIdx.x >> 6;
     tile = reinterpret_cast<float *>(after_tables + wave * kTileBytes);
-    const int obytes = out_buffer_bytes(a.out_cap, a.out_kind == 0 ? 1 : 4);
+    const int obytes = out_buffer_bytes(a.out_cap, a.out_kind == 0 ? 1 : 4, TR);
     obuf = reinterpret_cast<uint8_t *>(after_tables) + a.waves * kTileBytes + wave * obytes;
 }
 

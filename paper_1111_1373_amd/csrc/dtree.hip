@@ -176,6 +176,7 @@ struct Plan {
     int blocks_per_cu = 0;
     int lds_bytes = 0;
     int out_cap = 0;          // single-tree kernels: result tiles buffered per wavefront
+    int tile_rows = dtree::kTileRows;   // records per wavefront tile
     int tables_in_lds = 0;
     dt_status status = DT_ERR_UNSUPPORTED;
     std::string why;
@@ -191,12 +192,16 @@ std::vector<const void *> g_prepared;
 // wavefront up to 16 per CU (uint8 records of 64 features: 207 us with 16 against 282 us
 // with 8); with 16 KiB tiles (64 fp32 features) 64 KiB in flight is again the better
 // point: 4 wavefronts keep a larger result buffer next to the tables and measure 640 us
-// on 16,777,216 x 64 records against 674 us with 5.  The path reduction is latency-bound
-// and takes as many wavefronts as fit, up to 8.
-int target_waves_per_cu(int algo, int tile_bytes) {
+// on 16,777,216 x 64 records against 674 us with 5.  Its 64-lane groups (32-record tiles)
+// issue 64 slot evaluations per record and level and gain up to 96 KiB of tiles per CU:
+// 730 us with 12 wavefronts of 8 KiB tiles against 775 us with 8 on the same records.
+// The path reduction is latency-bound and takes as many wavefronts as fit, up to 8.
+int target_waves_per_cu(int algo, int tile_bytes, int tile_rows) {
     const int hbm = std::max(2, std::min(32, (64 * 1024) / tile_bytes));
     if (algo == DT_ALGO_DATA) return hbm;
-    if (algo == DT_ALGO_SPECULATIVE) return std::min(16, hbm);
+    if (algo == DT_ALGO_SPECULATIVE)
+        return tile_rows < dtree::kTileRows ? std::min(16, (96 * 1024) / tile_bytes)
+                                            : std::min(16, hbm);
     return 8;
 }
 
@@ -225,9 +230,12 @@ dt_status make_plan(const DeviceCaps &caps, int algo, int elem_type, int row_str
                     int load_mode, int depth, int64_t table_bytes, int out_bytes,
                     int waves_per_cu, Plan *plan) {
     const int path_bytes = algo == DT_ALGO_PATH ? dtree::kPathIntsPerWave * 4 : 0;
-    const int record_tile_bytes = dtree::tile_bytes_for(row_stride, elem_type);
+    const int tile_rows =
+        dtree::tile_rows_for(algo, depth, row_stride * dtree::elem_bytes(elem_type));
+    plan->tile_rows = tile_rows;
+    const int record_tile_bytes = dtree::tile_bytes_for(row_stride, elem_type, tile_rows);
     const int tile_bytes = record_tile_bytes + path_bytes;
-    const int res_bytes = dtree::kTileRows * out_bytes;   // one tile of results
+    const int res_bytes = tile_rows * out_bytes;   // one tile of results
     if (tile_bytes + res_bytes > caps.lds_per_block) {
         plan->why = "one record tile exceeds the workgroup LDS";
         return plan->status = DT_ERR_UNSUPPORTED;
@@ -246,12 +254,14 @@ dt_status make_plan(const DeviceCaps &caps, int algo, int elem_type, int row_str
     if (plan->status != DT_OK) return plan->status;
 
     const int target =
-        waves_per_cu > 0 ? waves_per_cu : target_waves_per_cu(algo, record_tile_bytes);
+        waves_per_cu > 0 ? waves_per_cu : target_waves_per_cu(algo, record_tile_bytes, tile_rows);
     // Try every workgroup size and count per CU; keep the shape reaching the most resident
     // wavefronts up to the target (registers and the LDS both limit residency); on ties
     // prefer larger workgroups (fewer table copies), then a larger result buffer.
     int best = 0, best_cap = 0;
-    for (int w = std::min(dtree::kMaxWavesPerBlock, target); w >= 1; --w) {
+    const int max_waves =
+        dtree::tree_max_waves(algo, depth, row_stride * dtree::elem_bytes(elem_type));
+    for (int w = std::min(max_waves, target); w >= 1; --w) {
         for (int bpc = (target + w - 1) / w; bpc >= 1; --bpc) {
             const int budget = std::min(caps.lds_per_block, caps.lds_per_cu / bpc);
             if (table_lds + w * (tile_bytes + res_bytes) > budget) continue;
@@ -357,12 +367,13 @@ uint32_t magic_div(int32_t d) {
     return d >= 2 ? uint32_t(((uint64_t(1) << 32) + uint64_t(d) - 1) / uint64_t(d)) : 0u;
 }
 
-dtree::Rows make_rows(const void *d_x, int elem_type, int64_t n, int64_t ld, int32_t n_features) {
+dtree::Rows make_rows(const void *d_x, int elem_type, int64_t n, int64_t ld, int32_t n_features,
+                      int tile_rows = dtree::kTileRows) {
     dtree::Rows r{};
     r.x = d_x;
     r.n = n;
     r.ld = ld;
-    r.n_tiles = (n + dtree::kTileRows - 1) / dtree::kTileRows;
+    r.n_tiles = (n + tile_rows - 1) / tile_rows;
     r.n_features = n_features;
     r.magic_f = magic_div(n_features);
     r.n_words = n_features * dtree::elem_bytes(elem_type) / 4;   // used by vector loads only
@@ -405,7 +416,7 @@ dt_status classify_impl(const dt_tree *tree, const void *d_x, dt_dtype x_type, i
     const Encoding &enc = tree->enc[encoding_of(algo)];
 
     dtree::KArgs a{};
-    a.in = make_rows(d_x, x_type, n, ld, tree->n_features);
+    a.in = make_rows(d_x, x_type, n, ld, tree->n_features, plan.tile_rows);
     a.slots = enc.d_slots[x_type];
     a.exits = out_kind == DT_OUT_LEAF_I32 ? enc.d_exit_leaf : enc.d_exit_class;
     a.slot_bytes = int32_t(enc.slot_bytes[x_type]);
@@ -959,6 +970,7 @@ dt_status dt_tree_launch_info(const dt_tree *t, const void *d_x, dt_dtype x_type
     info->result_buffer_tiles = plan.out_cap;
     info->tables_in_lds = plan.tables_in_lds;
     info->load_mode = mode;
+    info->tile_rows = plan.tile_rows;
     return DT_OK;
 }
 

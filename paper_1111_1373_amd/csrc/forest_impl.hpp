@@ -130,7 +130,9 @@ __global__ void __launch_bounds__(64 * forest_max_waves(SD == 0 ? 0 : 1, SD, RS)
         if constexpr (SD == 0) {
             return dev::walk_data<kXF32, kStride>(sl, ex, a.depth, levels, row, sw);
         } else {
-            const dev::Spec<kXF32, RS, SD> spec(lane);
+            using Spec = dev::Spec<kXF32, RS, SD>;
+            static_assert(Spec::kLayout == dev::kRowMajor, "forest tiles are staged row-major");
+            const Spec spec(lane);
             const Slot root = sl[spec.j];
             return spec.run(sl, ex, levels, root, tile);   // int32 codes (EX is int32 here)
         }

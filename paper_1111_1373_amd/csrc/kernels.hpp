@@ -7,6 +7,8 @@
 
 namespace dtree {
 
+enum KernelAlgo { kAlgoData = 0, kAlgoSpec = 1, kAlgoPath = 2 };
+
 constexpr int kTileRows = 64;          // records per wavefront tile (one per lane)
 constexpr int kMaxRowStride = 256;     // LDS row stride limit in floats (n_features <= 256)
 constexpr int kMaxWavesPerBlock = 8;   // kernels are built for <= 512 threads, except:
@@ -59,8 +61,27 @@ struct KArgs {
 // Path-reduction kernel: per wavefront, 64/S segments of 2S path entries (S lanes each).
 constexpr int kPathIntsPerWave = 128;
 
-// LDS bytes of one wavefront's result buffer: cap tiles of 64 results of out_bytes each.
-__host__ __device__ inline int out_buffer_bytes(int cap, int out_bytes) { return cap * kTileRows * out_bytes; }
+// Records per wavefront tile of a kernel: 64 (one per lane), except for the speculative
+// kernel with 64-slot windows (depth 6) on rows of at least 32 bytes in the LDS.  That
+// kernel reads one record row per round, so a tile of 32 records serves it as well while
+// taking half the LDS, and twice as many wavefronts then fit next to its window tables.
+// (Rows under 32 bytes keep 64 records: 16-byte staging needs one vector per lane.)
+__host__ __device__ constexpr int tile_rows_for(int algo, int depth, int row_bytes) {
+    return algo == kAlgoSpec && depth == 6 && row_bytes >= 32 ? 32 : kTileRows;
+}
+
+// Largest workgroup of a single-tree kernel instance, in wavefronts: 8, or 16 for the
+// speculative walk on 32-record tiles, whose registers (at most 128 per lane) fit 16
+// wavefronts per CU and whose small tiles leave the LDS room for them.
+__host__ __device__ constexpr int tree_max_waves(int algo, int depth, int row_bytes) {
+    return tile_rows_for(algo, depth, row_bytes) < kTileRows ? 16 : kMaxWavesPerBlock;
+}
+
+// LDS bytes of one wavefront's result buffer: cap tiles of `tile_rows` results of
+// out_bytes each.
+__host__ __device__ inline int out_buffer_bytes(int cap, int out_bytes, int tile_rows = kTileRows) {
+    return cap * tile_rows * out_bytes;
+}
 
 // Forest kernel arguments.  Tree k's tables are the bytes [off_k, off_k + slot_bytes_k)
 // (slots) followed by its exit codes (int16 when every code of the forest fits, else
@@ -80,8 +101,6 @@ struct FArgs {
     int32_t out_kind;        // 0: uint8 output, 1: int32 output
     void *out;
 };
-
-enum KernelAlgo { kAlgoData = 0, kAlgoSpec = 1, kAlgoPath = 2 };
 
 // How record tiles are read from HBM.
 enum LoadMode {
@@ -124,9 +143,9 @@ hipError_t launch_kernel(const void *fn, const KArgs &args, int blocks, int lds_
 hipError_t launch_forest(const void *fn, const FArgs &args, int blocks, int lds_bytes,
                          hipStream_t stream);
 
-// LDS bytes of one record tile: 64 rows of `row_stride` elements of `elem_type`.
-inline int tile_bytes_for(int row_stride, int elem_type) {
-    return kTileRows * row_stride * elem_bytes(elem_type);
+// LDS bytes of one record tile: tile_rows rows of `row_stride` elements of `elem_type`.
+inline int tile_bytes_for(int row_stride, int elem_type, int tile_rows = kTileRows) {
+    return tile_rows * row_stride * elem_bytes(elem_type);
 }
 
 // Dynamic LDS of a workgroup of `waves` wavefronts: tables, one record tile per wavefront,

@@ -44,7 +44,8 @@ __global__ void __launch_bounds__(512) data_kernel(KArgs a) {
 }
 
 template <int XT, int RS, int LOAD, bool TAB_LDS, int D>
-__global__ void __launch_bounds__(512) spec_kernel(KArgs a) {
+__global__ void __launch_bounds__(64 * tree_max_waves(kAlgoSpec, D, RS * int(sizeof(typename dev::Elem<XT>::T))))
+spec_kernel(KArgs a) {
     using T = typename dev::Elem<XT>::T;
     using NS = typename dev::Node<XT>::S;
     extern __shared__ int4 lds[];
@@ -52,13 +53,15 @@ __global__ void __launch_bounds__(512) spec_kernel(KArgs a) {
     const int32_t *exits;
     char *tiles = dev::bind_tables<TAB_LDS>(a, lds, slots, exits);
     const int lane = threadIdx.x & 63;
+    constexpr int TR = tile_rows_for(kAlgoSpec, D, RS * int(sizeof(T)));
     float *tile;
     uint8_t *obuf;
-    dev::wave_buffers<XT, RS>(a, tiles, tile, obuf);
-    const dev::Spec<XT, RS, D> spec(lane);
+    dev::wave_buffers<XT, RS, TR>(a, tiles, tile, obuf);
+    using Spec = dev::Spec<XT, RS, D, TR>;
+    const Spec spec(lane);
     const NS root = slots[spec.j];   // window 0 is shared by every record
     const T *el = reinterpret_cast<const T *>(tile);
-    dev::tile_loop<XT, RS, LOAD>(a, tile, obuf, lane, [&](int64_t) -> int32_t {
+    dev::tile_loop<XT, RS, LOAD, Spec::kLayout, TR>(a, tile, obuf, lane, [&](int64_t) -> int32_t {
         return ~spec.run(slots, exits, a.levels, root, el);
     });
 }

@@ -71,7 +71,7 @@ class PipelineStats(ctypes.Structure):
 class LaunchInfo(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "waves_per_workgroup", "workgroups_per_cu", "lds_bytes", "result_buffer_tiles",
-        "tables_in_lds", "load_mode")]
+        "tables_in_lds", "load_mode", "tile_rows")]
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}
