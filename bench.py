@@ -39,7 +39,7 @@ PAPER_CONTEXT = {"speculative_us": 404.466, "data_us": 538.235, "ratio": 404.466
 KERNEL_SOURCES = {"data": ("kernels.hip", "kernels_impl.hpp"),
                   "speculative": ("kernels.hip", "kernels_impl.hpp"),
                   "path": ("path.hip",),
-                  "forest": ("forest.hip", "forest_impl.hpp", "forest_ex16.hip")}
+                  "forest": ("forest.hip", "forest_impl.hpp", "forest_ex16.hip", "forest_packed.hip")}
 
 
 def kernel_source_hash(algo: str) -> str:

@@ -19,7 +19,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libdtree.so")
 OBJDIR = os.path.join(HERE, "_build")
 SOURCES = ["dtree.hip", "kernels.hip", "kernels_f16.hip", "kernels_bf16.hip", "kernels_u8.hip",
-           "forest.hip", "forest_ex16.hip", "probe.hip", "path.hip", "encode.cpp", "pipeline.cpp"]
+           "forest.hip", "forest_ex16.hip", "forest_packed.hip", "probe.hip", "path.hip", "encode.cpp", "pipeline.cpp"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

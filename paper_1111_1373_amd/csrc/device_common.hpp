@@ -37,6 +37,14 @@ struct alignas(16) Slot2 {
     Slot l, r;
 };
 
+// Exit codes packed into the window's bottom slots (forest data walk): the 32-bit word of
+// a slot p in [S/2, S) holds the feature's byte offset in bits 0-9 and the exit codes of
+// its children 2p and 2p+1 (11-bit two's complement) in bits 10-20 and 21-31; slots
+// above the bottom level hold the byte offset alone.  The exit is then known from the
+// last slot of the window, with no read of an exit table.
+struct PackedExits {};
+constexpr int kPackedFeatureMask = 0x3FF;
+
 // Word swizzle of row r for rows of RSW 4-byte words.
 template <int RSW>
 __device__ __forceinline__ int swz(int r) {
@@ -230,6 +238,8 @@ struct VecTile {
         }
     }
 
+    __device__ __forceinline__ void store_col_major(float *tile, int lane) const;
+
     // Any tile, including the partial last one.
     __device__ __forceinline__ void load_tail(const Rows &in, int64_t tile, int lane) {
         load_clamped(in, tile, lane, (valid_rows<TR>(in, tile) * in.n_words) >> 2);
@@ -237,7 +247,11 @@ struct VecTile {
 
     template <int LAYOUT = kRowMajor>
     __device__ __forceinline__ void store(const Rows &in, float *tile, int lane) const {
-        if constexpr (EXACT) {
+        if constexpr (EXACT && LAYOUT == kColMajor && RSW <= 32) {
+            // (wider rows keep the plain stores: the butterfly's 2 x RSW registers would
+            // not fit the forest kernel's 128)
+            store_col_major(tile, lane);
+        } else if constexpr (EXACT) {
             constexpr int sh = __builtin_ctz(RSW);
 #pragma unroll
             for (int k = 0; k < kVec; ++k) {
@@ -258,6 +272,50 @@ struct VecTile {
         }
     }
 };
+
+// Column-major stores of a full exact tile without bank conflicts (64-record tiles).  With
+// L = RSW / 4 lanes per row, lane l = a*L + b holds in v[k] the words 4b..4b+3 of row
+// k*(64/L) + a.  Storing one register at a time would send 64 lanes to only 64/L rows,
+// i.e. 64/L banks of a column-major tile (an L-way conflict).  Store j instead takes
+// v[b ^ j] in every lane: its rows (b ^ j)*(64/L) + a are 64 distinct rows, so each store
+// touches every bank once.  The per-lane choice of register is an XOR butterfly of selects
+// (log2 L stages of conditional swaps), after which w[j] == v[b ^ j].
+template <int RSW, bool EXACT, int TR>
+__device__ __forceinline__ void store_col_major_tile(const f32x4 (&v)[RSW / 4], float *tile, int lane) {
+    constexpr int L = RSW / 4;                  // lanes per row = vectors per lane
+    constexpr int R = 64 / L;                   // rows per load instruction
+    static_assert(TR == kTileRows && L >= 1 && (L & (L - 1)) == 0, "64-record exact tiles");
+    const int a = lane / L, b = lane % L;
+    f32x4 w[L];
+#pragma unroll
+    for (int k = 0; k < L; ++k) w[k] = v[k];
+#pragma unroll
+    for (int bit = 1; bit < L; bit <<= 1) {
+        const bool swap = (b & bit) != 0;
+#pragma unroll
+        for (int k = 0; k < L; ++k) {
+            if (k & bit) continue;
+            const f32x4 lo = w[k], hi = w[k | bit];
+            w[k] = swap ? hi : lo;
+            w[k | bit] = swap ? lo : hi;
+        }
+    }
+    // word (4b + i)*64 + (b ^ j)*R + a of the tile
+    float *col = tile + (4 * b) * kTileRows + a;
+#pragma unroll
+    for (int j = 0; j < L; ++j) {
+        float *dst = col + (b ^ j) * R;
+        dst[0 * kTileRows] = w[j].x;
+        dst[1 * kTileRows] = w[j].y;
+        dst[2 * kTileRows] = w[j].z;
+        dst[3 * kTileRows] = w[j].w;
+    }
+}
+
+template <int RSW, bool EXACT, int TR>
+__device__ __forceinline__ void VecTile<RSW, EXACT, TR>::store_col_major(float *tile, int lane) const {
+    store_col_major_tile<RSW, EXACT, TR>(v, tile, lane);
+}
 
 // Vectorised staging of wide rows (RSW > 64 words) in chunks of 16 vectors per lane,
 // without prefetch (loads clamped to the valid vectors as in VecTile).
@@ -397,33 +455,72 @@ __device__ __forceinline__ int32_t walk_data(const typename Node<XT>::S *slots,
     return code;
 }
 
+// The first three slots of a tree's window 0 (the root and its two children) as
+// wavefront-uniform values, read from the tree's tables in global memory through the
+// constant address space (one scalar load).
+struct TopSlots {
+    Slot s1, s2, s3;
+};
+
+__device__ __forceinline__ TopSlots top_slots(const char *window0) {
+    typedef int v8i __attribute__((ext_vector_type(8)));
+    typedef const __attribute__((address_space(4))) v8i ConstV8i;
+    const v8i v = *((ConstV8i *)(window0));
+    return TopSlots{Slot{__int_as_float(v[2]), v[3]}, Slot{__int_as_float(v[4]), v[5]},
+                    Slot{__int_as_float(v[6]), v[7]}};
+}
+
 // Data decomposition over K trees at once (forests): the K walks of one record are
 // independent, so interleaving them keeps K LDS dependency chains in flight per lane.
-// Tree i's tables start at base[i]; all trees share the window depth D.
+// Tree i's tables start at base[i] (LDS or global memory) and, in global memory, at
+// gbase[i]; all trees share the window depth D.
 template <int K, int STRIDE = 1, class EX = int32_t>
-__device__ __forceinline__ void walk_data_k(const char *const (&base)[K], const int (&slot_bytes)[K],
-                                            const int (&levels)[K], int D, const float *row,
-                                            int sw, int32_t (&code)[K]) {
+__device__ __forceinline__ void walk_data_k(const char *const (&base)[K],
+                                            const char *const (&gbase)[K],
+                                            const int (&slot_bytes)[K], const int (&levels)[K],
+                                            int D, const float *row, int sw, int32_t (&code)[K]) {
     // K independent chains already hide the LDS latency, so each level reads just the
     // node's own 8-byte slot (no lookahead): fewer LDS bytes and bank conflicts per step.
     const int S = 1 << D;
-    int w[K];
+    int w[K], p[K];
     int max_levels = 0;
 #pragma unroll
     for (int i = 0; i < K; ++i) {
         w[i] = 0;
+        p[i] = 1;
         code[i] = 0;
         max_levels = levels[i] > max_levels ? levels[i] : max_levels;
     }
-    for (int level = 0; level < max_levels; ++level) {
-        const Slot *win[K];
-        int p[K];
+    // Every walk starts at the root of window 0, and its first two nodes (slot 1, then slot
+    // 2 or 3) are the same for every lane: they come from scalar registers, which saves
+    // two of the LDS slot reads per tree (the LDS pipe bounds this walk).  With packed
+    // exits the window's bottom level always comes from the LDS (its slots carry the exits).
+    constexpr bool kPacked = std::is_same<EX, PackedExits>::value;
+    int k0 = 0;
+    if (D >= (kPacked ? 3 : 2)) {
+        TopSlots top[K];
+#pragma unroll
+        for (int i = 0; i < K; ++i) top[i] = top_slots(gbase[i]);
+        bool r0[K];
 #pragma unroll
         for (int i = 0; i < K; ++i) {
-            win[i] = reinterpret_cast<const Slot *>(base[i]) + (w[i] << D);
-            p[i] = 1;
+            const float xv = feature_at<kXF32, STRIDE>(row, top[i].s1, sw);
+            r0[i] = !(xv < top[i].s1.t);
+            p[i] = heap_step(1, r0[i]);
         }
-        for (int k = 0; k < D; ++k) {
+#pragma unroll
+        for (int i = 0; i < K; ++i) {
+            const Slot s = r0[i] ? top[i].s3 : top[i].s2;
+            const float xv = feature_at<kXF32, STRIDE>(row, s, sw);
+            p[i] = heap_step(p[i], !(xv < s.t));
+        }
+        k0 = 2;
+    }
+    for (int level = 0; level < max_levels; ++level) {
+        const Slot *win[K];
+#pragma unroll
+        for (int i = 0; i < K; ++i) win[i] = reinterpret_cast<const Slot *>(base[i]) + (w[i] << D);
+        for (int k = level == 0 ? k0 : 0; k < (kPacked ? D - 1 : D); ++k) {
 #pragma unroll
             for (int i = 0; i < K; ++i) {
                 const Slot s = win[i][p[i]];
@@ -431,13 +528,24 @@ __device__ __forceinline__ void walk_data_k(const char *const (&base)[K], const 
                 p[i] = heap_step(p[i], !(xv < s.t));
             }
         }
-        // Every chain reads its exit, finished or not (a finished chain re-walked its last
-        // window, so the index stays inside that window's exits), and the K reads are
-        // issued together; a chain still running at this level has level < levels[i].
+        // Every chain takes its exit, finished or not (a finished chain re-walked its last
+        // window, so the index stays inside that window's exits), the K reads issued
+        // together; a chain still running at this level has level < levels[i].
         int32_t c[K];
+        if constexpr (kPacked) {
+            // the bottom step: the slot's word names the feature and both exits
 #pragma unroll
-        for (int i = 0; i < K; ++i)
-            c[i] = int32_t(reinterpret_cast<const EX *>(base[i] + slot_bytes[i])[(w[i] << D) + p[i] - S]);
+            for (int i = 0; i < K; ++i) {
+                const Slot s = win[i][p[i]];
+                const Slot node{s.t, s.f & kPackedFeatureMask};
+                const float xv = feature_at<kXF32, STRIDE>(row, node, sw);
+                c[i] = !(xv < s.t) ? (s.f >> 21) : ((s.f << 11) >> 21);
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < K; ++i)
+                c[i] = int32_t(reinterpret_cast<const EX *>(base[i] + slot_bytes[i])[(w[i] << D) + p[i] - S]);
+        }
         bool all_done = true;
 #pragma unroll
         for (int i = 0; i < K; ++i) {
@@ -445,6 +553,7 @@ __device__ __forceinline__ void walk_data_k(const char *const (&base)[K], const 
             w[i] = live && c[i] >= 0 ? c[i] : w[i];
             code[i] = live ? c[i] : code[i];
             all_done = all_done && code[i] < 0;
+            p[i] = 1;
         }
         if (__all(all_done)) break;
     }

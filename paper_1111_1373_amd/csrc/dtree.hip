@@ -333,7 +333,8 @@ struct ForestEncoding {
     int64_t max_tree_bytes = 0;
     int32_t chunk_lds_bytes = 0; // LDS reserved for one chunk (0: tables read in place)
     int32_t waves = 0;           // wavefronts per workgroup (one tile each)
-    bool exit16 = false;         // exit codes stored as int16
+    int exit_mode = 0;           // exit codes: int32 table (0), int16 table (1), or packed
+                                 // into the windows' bottom slots (2)
 };
 
 void free_forest_encoding(ForestEncoding *e) {
@@ -523,17 +524,23 @@ void encode_forest(const dt_node *nodes, const int32_t *offsets, int32_t n_trees
     bytes->clear();
     std::vector<dtree::WindowTables> wts(static_cast<size_t>(n_trees));
     // Exit codes (next window ids, and results -(class + 1)) of the data decomposition are
-    // stored as int16 when every code of the forest fits: a third less table per tree, so
-    // more trees share a chunk.  (The speculative walk keeps int32 codes: its int16
-    // instance needs more registers than 16 wavefronts per CU leave it.)
-    bool fits16 = algo == DT_ALGO_DATA;
+    // packed into the spare bits of the windows' bottom slots when every code of the forest
+    // fits 11 bits (the feature's byte offset, at most 1020, takes the low 10): the tables
+    // then hold slots only, a fifth less than with int16 codes (four complete depth-10
+    // trees per 32 KiB chunk instead of three), and the walk reads no exit table.  Failing
+    // that they are int16 when every code fits, else int32.  (The speculative walk keeps
+    // int32 codes: its narrower instances need more registers than 16 wavefronts per CU
+    // leave it.)
+    bool fits11 = algo == DT_ALGO_DATA, fits16 = algo == DT_ALGO_DATA;
     for (int32_t k = 0; k < n_trees; ++k) {
         dtree::build_windows(nodes + offsets[k], shapes[size_t(k)], depth, &wts[size_t(k)]);
-        for (int32_t c : wts[size_t(k)].exit_class)
+        for (int32_t c : wts[size_t(k)].exit_class) {
+            fits11 = fits11 && c >= -1024 && c <= 1023;
             fits16 = fits16 && c >= INT16_MIN && c <= INT16_MAX;
+        }
     }
-    enc->exit16 = fits16;
-    const int64_t exit_size = fits16 ? 2 : 4;
+    enc->exit_mode = fits11 ? 2 : fits16 ? 1 : 0;
+    const int64_t exit_size = enc->exit_mode == 2 ? 0 : enc->exit_mode == 1 ? 2 : 4;
     for (int32_t k = 0; k < n_trees; ++k) {
         const dtree::WindowTables &wt = wts[size_t(k)];
         const int64_t n_slots = int64_t(wt.n_windows) * wt.slots;
@@ -541,17 +548,25 @@ void encode_forest(const dt_node *nodes, const int32_t *offsets, int32_t n_trees
         const int64_t off = int64_t(bytes->size());
         bytes->resize(size_t(off + sb + eb), 0);
         unsigned char *p = bytes->data() + off;
+        const int64_t S = wt.slots;
         for (int64_t i = 0; i < n_slots; ++i) {
-            const int32_t fb = 4 * wt.feature[size_t(i)];   // byte offset in an fp32 row
+            int32_t fb = 4 * wt.feature[size_t(i)];   // byte offset in an fp32 row
+            const int64_t q = i % S;                  // heap position in the window
+            if (enc->exit_mode == 2 && q >= S / 2) {  // bottom level: its children's exits
+                const int64_t e = i - q + 2 * q - S;  // exit of child 2q in this window
+                const uint32_t lo = uint32_t(wt.exit_class[size_t(e)]) & 0x7FFu;
+                const uint32_t hi = uint32_t(wt.exit_class[size_t(e + 1)]) & 0x7FFu;
+                fb = int32_t(uint32_t(fb) | lo << 10 | hi << 21);
+            }
             std::memcpy(p + 8 * i, &wt.threshold[size_t(i)], 4);
             std::memcpy(p + 8 * i + 4, &fb, 4);
         }
-        if (fits16) {
+        if (enc->exit_mode == 1) {
             for (int64_t i = 0; i < n_slots; ++i) {
                 const int16_t c = int16_t(wt.exit_class[size_t(i)]);
                 std::memcpy(p + sb + 2 * i, &c, 2);
             }
-        } else {
+        } else if (enc->exit_mode == 0) {
             std::memcpy(p + sb, wt.exit_class.data(), size_t(n_slots * 4));
         }
         enc->trees[size_t(k)] = int4{int(off), int(sb), wt.levels, 0};
@@ -645,7 +660,7 @@ dt_status plan_forest(const DeviceCaps &caps, int algo, int row_stride, int load
                       int vote_words, const ForestEncoding &enc, Plan *plan) {
     const bool tab_lds = enc.chunk_lds_bytes > 0;
     plan->fn = dtree::forest_kernel_for(algo, row_stride, load_mode, tab_lds, vote_words,
-                                        enc.depth, enc.exit16);
+                                        enc.depth, enc.exit_mode);
     if (!plan->fn) {
         plan->why = "no forest kernel instance for this configuration";
         return plan->status = DT_ERR_UNSUPPORTED;

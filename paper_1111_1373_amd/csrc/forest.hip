@@ -5,8 +5,11 @@
 namespace dtree {
 
 const void *forest_kernel_for(int algo, int row_stride, int load_mode, bool tables_in_lds,
-                              int vote_words, int depth, bool exit16) {
-    if (exit16)
+                              int vote_words, int depth, int exit_mode) {
+    if (exit_mode == 2)
+        return forest_kernel_for_packed(algo, row_stride, load_mode, tables_in_lds, vote_words,
+                                        depth);
+    if (exit_mode == 1)
         return forest_kernel_for_ex16(algo, row_stride, load_mode, tables_in_lds, vote_words,
                                       depth);
     return forest_kernel_for_ex<int32_t>(algo, row_stride, load_mode, tables_in_lds,

@@ -104,7 +104,8 @@ __device__ __forceinline__ void copy_chunk_staged(const FArgs &a, int4 *tab, con
 }
 
 // SD = 0: data decomposition; SD > 0: speculative decomposition with window depth SD.
-// EX: exit codes stored as int32, or int16 where every code of the forest fits.
+// EX: exit codes stored as int32, int16 where every code of the forest fits, or packed
+// into the windows' bottom slots (dev::PackedExits) where every code fits 11 bits.
 template <class EX, int RS, int LOAD, bool TAB_LDS, int NV, int SD>
 __global__ void __launch_bounds__(64 * forest_max_waves(SD == 0 ? 0 : 1, SD, RS)) forest_kernel(FArgs a) {
     extern __shared__ int4 lds[];
@@ -123,19 +124,16 @@ __global__ void __launch_bounds__(64 * forest_max_waves(SD == 0 ? 0 : 1, SD, RS)
     const int sw = SD == 0 ? 0 : dev::swz<RS>(lane);
     const int64_t n_groups = (a.in.n_tiles + a.waves - 1) / a.waves;
 
-    // Exit code of this lane's record for the tree whose tables start at `base`.
+    // Speculative decomposition: exit code of this lane's record for the tree whose tables
+    // start at `base` (int32 codes).
     auto eval_tree = [&](const char *base, int levels, int slot_bytes) -> int32_t {
         const Slot *sl = reinterpret_cast<const Slot *>(base);
-        const EX *ex = reinterpret_cast<const EX *>(base + slot_bytes);
-        if constexpr (SD == 0) {
-            return dev::walk_data<kXF32, kStride>(sl, ex, a.depth, levels, row, sw);
-        } else {
-            using Spec = dev::Spec<kXF32, RS, SD>;
-            static_assert(Spec::kLayout == dev::kRowMajor, "forest tiles are staged row-major");
-            const Spec spec(lane);
-            const Slot root = sl[spec.j];
-            return spec.run(sl, ex, levels, root, tile);   // int32 codes (EX is int32 here)
-        }
+        const int32_t *ex = reinterpret_cast<const int32_t *>(base + slot_bytes);
+        using Spec = dev::Spec<kXF32, RS, SD == 0 ? 2 : SD>;
+        static_assert(Spec::kLayout == dev::kRowMajor, "forest tiles are staged row-major");
+        const Spec spec(lane);
+        const Slot root = sl[spec.j];
+        return spec.run(sl, ex, levels, root, tile);
     };
 
     // A forest whose tables form one chunk is copied once: the tables then stay for every
@@ -187,67 +185,44 @@ __global__ void __launch_bounds__(64 * forest_max_waves(SD == 0 ? 0 : 1, SD, RS)
                     }
                     __syncthreads();
                 }
-                if (active) {
-                    const char *cbase = reinterpret_cast<const char *>(tab);
-                    int k = ch.x;
-                    if constexpr (SD == 0) {
-                        // K trees of the chunk walked together from tree k
-                        auto walk_group = [&](auto kk, int k0) {
-                            constexpr int K = decltype(kk)::value;
-                            const char *base[K];
-                            int sb[K], lv[K];
-                            int32_t code[K];
+            }
+            if (!active) continue;
+            // tables of the chunk's trees: in the LDS chunk buffer (which starts at the
+            // chunk's byte offset ch.z of the tables), or in place
+            const char *cbase = TAB_LDS ? reinterpret_cast<const char *>(tab)
+                                        : reinterpret_cast<const char *>(a.tables);
+            const int cofs = TAB_LDS ? ch.z : 0;
+            int k = ch.x;
+            if constexpr (SD == 0) {
+                // K trees of the chunk walked together from tree k0
+                auto walk_group = [&](auto kk, int k0) {
+                    constexpr int K = decltype(kk)::value;
+                    const char *base[K], *gb[K];
+                    int sb[K], lv[K];
+                    int32_t code[K];
 #pragma unroll
-                            for (int i = 0; i < K; ++i) {
-                                const int4 d = read_const(a.trees, k0 + i);
-                                base[i] = cbase + (d.x - ch.z);
-                                sb[i] = d.y;
-                                lv[i] = d.z;
-                            }
-                            dev::walk_data_k<K, kStride, EX>(base, sb, lv, a.depth, row, sw, code);
+                    for (int i = 0; i < K; ++i) {
+                        const int4 d = read_const(a.trees, k0 + i);   // {byte_off, slot_bytes, levels, 0}
+                        base[i] = cbase + (d.x - cofs);
+                        gb[i] = reinterpret_cast<const char *>(a.tables) + d.x;
+                        sb[i] = d.y;
+                        lv[i] = d.z;
+                    }
+                    dev::walk_data_k<K, kStride, EX>(base, gb, sb, lv, a.depth, row, sw, code);
 #pragma unroll
-                            for (int i = 0; i < K; ++i) add_vote(votes, ~code[i]);
-                        };
-                        for (; k + kIlp <= ch.y; k += kIlp)
-                            walk_group(std::integral_constant<int, kIlp>(), k);
-                        if (ch.y - k == 3) {
-                            walk_group(std::integral_constant<int, 3>(), k);
-                            k += 3;
-                        } else if (ch.y - k == 2) {
-                            walk_group(std::integral_constant<int, 2>(), k);
-                            k += 2;
-                        }
-                    }
-                    for (; k < ch.y; ++k) {
-                        const int4 d = read_const(a.trees, k);   // {byte_off, slot_bytes, levels, 0}
-                        add_vote(votes, ~eval_tree(cbase + (d.x - ch.z), d.z, d.y));
-                    }
-                }
+                    for (int i = 0; i < K; ++i) add_vote(votes, ~code[i]);
+                };
+                for (; k + kIlp <= ch.y; k += kIlp) walk_group(std::integral_constant<int, kIlp>(), k);
+                if (ch.y - k == 3)
+                    walk_group(std::integral_constant<int, 3>(), k);
+                else if (ch.y - k == 2)
+                    walk_group(std::integral_constant<int, 2>(), k);
+                else if (ch.y - k == 1)
+                    walk_group(std::integral_constant<int, 1>(), k);
             } else {
-                if (active) {
-                    const char *gbase = reinterpret_cast<const char *>(a.tables);
-                    int k = ch.x;
-                    if constexpr (SD == 0) {
-                        for (; k + kIlp <= ch.y; k += kIlp) {
-                            const char *base[kIlp];
-                            int sb[kIlp], lv[kIlp];
-                            int32_t code[kIlp];
-#pragma unroll
-                            for (int i = 0; i < kIlp; ++i) {
-                                const int4 d = read_const(a.trees, k + i);
-                                base[i] = gbase + d.x;
-                                sb[i] = d.y;
-                                lv[i] = d.z;
-                            }
-                            dev::walk_data_k<kIlp, kStride, EX>(base, sb, lv, a.depth, row, sw, code);
-#pragma unroll
-                            for (int i = 0; i < kIlp; ++i) add_vote(votes, ~code[i]);
-                        }
-                    }
-                    for (; k < ch.y; ++k) {
-                        const int4 d = read_const(a.trees, k);
-                        add_vote(votes, ~eval_tree(gbase + d.x, d.z, d.y));
-                    }
+                for (; k < ch.y; ++k) {
+                    const int4 d = read_const(a.trees, k);   // {byte_off, slot_bytes, levels, 0}
+                    add_vote(votes, ~eval_tree(cbase + (d.x - cofs), d.z, d.y));
                 }
             }
         }
@@ -261,7 +236,7 @@ template <class EX, int RS, int LOAD, bool TAB_LDS, int NV>
 const void *for_votes(int algo, int depth) {
     if (algo == kAlgoData)
         return reinterpret_cast<const void *>(&forest_kernel<EX, RS, LOAD, TAB_LDS, NV, 0>);
-    if constexpr (sizeof(EX) == 4) {   // int16 codes: data walk only
+    if constexpr (std::is_same<EX, int32_t>::value) {   // narrower codes: data walk only
         if (depth == 2)
             return reinterpret_cast<const void *>(&forest_kernel<EX, RS, LOAD, TAB_LDS, NV, 2>);
         if (depth == 4)

@@ -127,12 +127,15 @@ const void *kernel_for_u8(int algo, int row_stride, int load_mode, bool tables_i
 const void *path_kernel_for(int row_stride, int load_mode, bool tables_in_lds, int depth);
 
 // Forest kernel instance; `vote_words` = 32-bit words of packed 8-bit counters
-// (2, 4 or 16 for up to 8, 16 or 64 classes); `exit16`: exit codes stored as int16.
+// (2, 4 or 16 for up to 8, 16 or 64 classes); `exit_mode`: exit codes stored as int32 (0)
+// or int16 (1) tables, or packed into the windows' bottom slots (2, data walk only).
 const void *forest_kernel_for(int algo, int row_stride, int load_mode, bool tables_in_lds,
-                              int vote_words, int depth, bool exit16);
-// The int16 instances (their own translation unit).
+                              int vote_words, int depth, int exit_mode);
+// The int16 and the packed instances (translation units of their own).
 const void *forest_kernel_for_ex16(int algo, int row_stride, int load_mode, bool tables_in_lds,
                                    int vote_words, int depth);
+const void *forest_kernel_for_packed(int algo, int row_stride, int load_mode,
+                                     bool tables_in_lds, int vote_words, int depth);
 
 // One-time per-instance setup (raise the dynamic LDS limit to the device maximum).
 hipError_t prepare_kernel(const void *fn, int max_lds_bytes);

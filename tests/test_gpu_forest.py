@@ -102,12 +102,14 @@ def test_large_trees_read_tables_in_place(dt):
     _check(dt, nodes, off, x, 16, 10)
 
 
-@pytest.mark.parametrize("n_internal", [32768, 32769])
+@pytest.mark.parametrize("n_internal", [1024, 1025, 32768, 32769])
 def test_exit_codes_at_the_int16_limit(dt, n_internal):
-    """Exit codes are stored as int16 when every code of the forest fits, else as int32.  A
-    chain cut into one-node windows has window ids 0 .. n_internal - 1: the largest is 32767
-    (int16) for 32,768 decision nodes and 32768 (int32) for 32,769.  Exits are rare (one
-    record in 10,000 per node), so a few percent of the records travel past window 32,767."""
+    """Exit codes are packed into the windows' bottom slots when every code of the forest
+    fits 11 bits, else stored as int16 when they fit 16, else as int32.  A chain cut into
+    one-node windows has window ids 0 .. n_internal - 1: the largest is 1023 (packed) for
+    1,024 decision nodes, 1024 (int16) for 1,025, 32767 (int16) for 32,768 and 32768
+    (int32) for 32,769.  Exits are rare (one record in 10,000 per node), so most records
+    travel the whole chain of 1,024 and a few percent past window 32,767."""
     r = np.random.Generator(np.random.PCG64(11))
     chain = W.chain_tree(r, n_internal, 8, 5, p_exit=1e-4)
     nodes, off = _forest([chain, W.complete_tree(r, 6, 8, 5)])
