@@ -455,19 +455,17 @@ __device__ __forceinline__ int32_t walk_data(const typename Node<XT>::S *slots,
     return code;
 }
 
-// The first three slots of a tree's window 0 (the root and its two children) as
-// wavefront-uniform values, read from the tree's tables in global memory through the
-// constant address space (one scalar load).
+// The root slot (slot 1) of a tree's window 0 as a wavefront-uniform value, read from the
+// tree's tables in global memory through the constant address space (one scalar load).
 struct TopSlots {
-    Slot s1, s2, s3;
+    Slot s1;
 };
 
 __device__ __forceinline__ TopSlots top_slots(const char *window0) {
-    typedef int v8i __attribute__((ext_vector_type(8)));
-    typedef const __attribute__((address_space(4))) v8i ConstV8i;
-    const v8i v = *((ConstV8i *)(window0));
-    return TopSlots{Slot{__int_as_float(v[2]), v[3]}, Slot{__int_as_float(v[4]), v[5]},
-                    Slot{__int_as_float(v[6]), v[7]}};
+    typedef int v4i_ __attribute__((ext_vector_type(4)));
+    typedef const __attribute__((address_space(4))) v4i_ ConstV4i_;
+    const v4i_ v = *((ConstV4i_ *)(window0));
+    return TopSlots{Slot{__int_as_float(v[2]), v[3]}};
 }
 
 // Data decomposition over K trees at once (forests): the K walks of one record are
@@ -491,30 +489,23 @@ __device__ __forceinline__ void walk_data_k(const char *const (&base)[K],
         code[i] = 0;
         max_levels = levels[i] > max_levels ? levels[i] : max_levels;
     }
-    // Every walk starts at the root of window 0, and its first two nodes (slot 1, then slot
-    // 2 or 3) are the same for every lane: they come from scalar registers, which saves
-    // two of the LDS slot reads per tree (the LDS pipe bounds this walk).  With packed
-    // exits the window's bottom level always comes from the LDS (its slots carry the exits).
+    // Every walk starts at the root of window 0, whose slot is the same for every lane: it
+    // comes from scalar registers, which saves one LDS slot read per tree (the LDS pipe is
+    // one of this walk's bounds).  The next level's two slots are cheaper to read from the
+    // LDS (two addresses: no bank conflicts) than to select from scalars (measured: four
+    // vector instructions more per tree, 419 against 408 us on a 32-tree forest).  With
+    // packed exits the window's bottom level always comes from the LDS (its slots carry the
+    // exits).
     constexpr bool kPacked = std::is_same<EX, PackedExits>::value;
     int k0 = 0;
-    if (D >= (kPacked ? 3 : 2)) {
-        TopSlots top[K];
-#pragma unroll
-        for (int i = 0; i < K; ++i) top[i] = top_slots(gbase[i]);
-        bool r0[K];
+    if (D >= (kPacked ? 2 : 1)) {
 #pragma unroll
         for (int i = 0; i < K; ++i) {
-            const float xv = feature_at<kXF32, STRIDE>(row, top[i].s1, sw);
-            r0[i] = !(xv < top[i].s1.t);
-            p[i] = heap_step(1, r0[i]);
+            const TopSlots top = top_slots(gbase[i]);
+            const float xv = feature_at<kXF32, STRIDE>(row, top.s1, sw);
+            p[i] = heap_step(1, !(xv < top.s1.t));
         }
-#pragma unroll
-        for (int i = 0; i < K; ++i) {
-            const Slot s = r0[i] ? top[i].s3 : top[i].s2;
-            const float xv = feature_at<kXF32, STRIDE>(row, s, sw);
-            p[i] = heap_step(p[i], !(xv < s.t));
-        }
-        k0 = 2;
+        k0 = 1;
     }
     for (int level = 0; level < max_levels; ++level) {
         const Slot *win[K];
@@ -533,18 +524,24 @@ __device__ __forceinline__ void walk_data_k(const char *const (&base)[K],
         // together; a chain still running at this level has level < levels[i].
         int32_t c[K];
         if constexpr (kPacked) {
-            // the bottom step: the slot's word names the feature and both exits
+            // the bottom step: the slot's word names the feature and both exits (the 11-bit
+            // field at bit 10 or bit 21, sign-extended)
 #pragma unroll
             for (int i = 0; i < K; ++i) {
                 const Slot s = win[i][p[i]];
-                const Slot node{s.t, s.f & kPackedFeatureMask};
+                const Slot node{s.t, int(__builtin_amdgcn_ubfe(uint32_t(s.f), 0, 10))};
                 const float xv = feature_at<kXF32, STRIDE>(row, node, sw);
-                c[i] = !(xv < s.t) ? (s.f >> 21) : ((s.f << 11) >> 21);
+                c[i] = __builtin_amdgcn_sbfe(s.f, !(xv < s.t) ? 21u : 10u, 11u);
             }
         } else {
 #pragma unroll
             for (int i = 0; i < K; ++i)
                 c[i] = int32_t(reinterpret_cast<const EX *>(base[i] + slot_bytes[i])[(w[i] << D) + p[i] - S]);
+        }
+        if (max_levels == 1) {            // one window per tree: the exits are the results
+#pragma unroll
+            for (int i = 0; i < K; ++i) code[i] = c[i];
+            break;
         }
         bool all_done = true;
 #pragma unroll

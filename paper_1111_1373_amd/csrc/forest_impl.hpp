@@ -96,10 +96,14 @@ __device__ __forceinline__ void copy_chunk_staged(const FArgs &a, int4 *tab, con
         v[q] = src[i < n16 ? i : n16 - 1];
     }
     __syncthreads();                                 // previous chunk no longer read
+    // unconditional writes too (a thread past the end writes the last word again, the same
+    // value its owner writes): with no branch around them, every load is waited for on one
+    // path, and the compiler needs no catch-all wait later (which, the vector-memory counter
+    // being in order, would also wait for the next record tiles' prefetch)
 #pragma unroll
     for (int q = 0; q < kStage; ++q) {
         const int i = int(threadIdx.x) + q * int(blockDim.x);
-        if (i < n16) dst[i] = v[q];
+        dst[i < n16 ? i : n16 - 1] = v[q];
     }
 }
 
@@ -165,10 +169,18 @@ __global__ void __launch_bounds__(64 * forest_max_waves(SD == 0 ? 0 : 1, SD, RS)
                 dev::stage_now<kXF32, RS, LOAD, kLayout>(a.in, tile, t, lane);
         }
         dev::wave_sync();
-        if constexpr (kPrefetch) {
-            const int64_t tn = t + int64_t(gridDim.x) * a.waves;
-            if (tn < n_full) buf.load_full(a.in, tn, lane);
-        }
+        // The next group's tiles are prefetched into registers: here, or, when the chunks
+        // are copied for every group, after the last chunk's copy (its loads would
+        // otherwise queue behind the prefetch on the in-order vector-memory counter, and the
+        // first chunk copy would wait for the prefetch to arrive from HBM).
+        const bool prefetch_late = TAB_LDS && a.n_chunks > 1;
+        auto prefetch_next = [&]() {
+            if constexpr (kPrefetch) {
+                const int64_t tn = t + int64_t(gridDim.x) * a.waves;
+                if (tn < n_full) buf.load_full(a.in, tn, lane);
+            }
+        };
+        if (!prefetch_late) prefetch_next();
 
         uint32_t votes[NV];
 #pragma unroll
@@ -184,6 +196,7 @@ __global__ void __launch_bounds__(64 * forest_max_waves(SD == 0 ? 0 : 1, SD, RS)
                         copy_chunk(a, tab, ch);
                     }
                     __syncthreads();
+                    if (c == a.n_chunks - 1) prefetch_next();
                 }
             }
             if (!active) continue;
