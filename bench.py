@@ -240,6 +240,11 @@ def main() -> int:
     ap.add_argument("--narrow-algos", default="data,speculative")
     ap.add_argument("--outer-reps", type=int, default=3,
                     help="calls per host-resident scheme timed for the outer time (0: skip)")
+    ap.add_argument("--spec-depths", default="1,2,3,4,5,6",
+                    help="speculative window depths timed on the headline workload ('' to skip)")
+    ap.add_argument("--configs", default="others",
+                    help="other workloads to time: 'others' (all but --config), 'none', or a "
+                         "comma-separated list of config numbers")
     ap.add_argument("--sweep", action="store_true",
                     help="tree geometry x record order sweep instead of the benchmark line")
     ap.add_argument("--sweep-geometries", default="all")
@@ -343,11 +348,11 @@ def main() -> int:
     # Cold-cache timing: inputs small enough to stay in the 256 MB last-level cache (MALL)
     # between launches are also timed after a 512 MiB write that evicts them.
     flush = None
-    if n * F * 4 < (1 << 30):
+    if n * F * 4 < (1 << 30) or args.configs != "none":
         flush = torch.empty(1 << 27, dtype=torch.float32, device="cuda")
 
-    def timed_cold(model, xd, algo, steps):
-        out = torch.empty(n, dtype=torch.uint8, device="cuda")
+    def timed_cold(model, xd, algo, steps, nrec=None):
+        out = torch.empty(n if nrec is None else nrec, dtype=torch.uint8, device="cuda")
         ks = []
         for _ in range(steps):
             flush.zero_()
@@ -360,9 +365,9 @@ def main() -> int:
             ks.append(e0.elapsed_time(e1) * 1e-3)
         return np.array(ks)
 
-    def timed(model, xd, algo, steps, warmup):
+    def timed(model, xd, algo, steps, warmup, nrec=None):
         """(wall seconds of `steps` launches, per-launch kernel seconds, labels)."""
-        out = torch.empty(n, dtype=torch.uint8, device="cuda")
+        out = torch.empty(n if nrec is None else nrec, dtype=torch.uint8, device="cuda")
         for _ in range(warmup):
             model.classify(xd, algo=algo, out=out, stream=stream)
         torch.cuda.synchronize()
@@ -397,7 +402,7 @@ def main() -> int:
                       else {"data": "data_kernel", "speculative": "spec_kernel",
                             "path": "path_kernel"}[algo],
         }
-        if flush is not None:
+        if flush is not None and n * F * 4 < (1 << 30):
             kc = timed_cold(tree, x, algo, args.steps)
             results[algo]["kernel_us_cold"] = {"avg": float(kc.mean()) * 1e6,
                                                "min": float(kc.min()) * 1e6,
@@ -410,6 +415,87 @@ def main() -> int:
         log(algo, json.dumps(results[algo]))
         if mism:
             log("PARITY FAILURE:", algo, mism, "mismatches")
+
+    def kernel_stats(ks):
+        return {"avg": float(ks.mean()) * 1e6, "min": float(ks.min()) * 1e6,
+                "max": float(ks.max()) * 1e6, "sd": float(ks.std()) * 1e6}
+
+    # Speculative window depths on the headline workload: depth 4 is the paper's 16-lane
+    # record groups (Section 4.2), depth 6 one 64-lane mask per window of 63 decision nodes
+    # with the tree cut into blocks of such windows (Sections 3.4 and 6).
+    depth_sweep = None
+    if not w.is_forest and args.spec_depths:
+        depth_sweep = {}
+        for d in [int(v) for v in args.spec_depths.split(",")]:
+            td = dt.Tree(w.nodes, w.n_features, w.n_classes, spec_window_depth=d,
+                         waves_per_cu=args.waves_per_cu)
+            wall, ks, got = timed(td, x, "speculative", args.steps, args.warmup)
+            kavg = float(ks.mean())
+            depth_sweep[str(d)] = {
+                "kernel_us": kernel_stats(ks), "kernel_samples_per_s": n / kavg,
+                "samples_per_s": n / (wall / args.steps),
+                "feature_frac_of_peak": feature_bytes / kavg / 1e9 / PEAK_HBM_GBPS,
+                "mismatches_vs_oracle": int((got != want).sum()),
+                "windows": td.info["spec_windows"], "window_levels": td.info["spec_levels"],
+                "table_bytes": td.info["spec_table_bytes"],
+                "launch": td.launch_info(x, algo="speculative", out_kind="class_u8")}
+            log("speculative depth", d, json.dumps(depth_sweep[str(d)]))
+            td.close()
+
+    # The other workloads (Table 1 reports every function built): each decomposition warm
+    # and after a cache-evicting write, checked against the oracle on all records.
+    configs = None
+    if args.configs != "none":
+        configs = {}
+        ks_list = ([k for k in (1, 2, 3, 4, 5) if k != args.config] if args.configs == "others"
+                   else [int(v) for v in args.configs.split(",")])
+        threads = max(1, min(16, len(os.sched_getaffinity(0))))
+        for k in ks_list:
+            wk = W.config(k)
+            xk_np = wk.features()
+            nk, Fk = xk_np.shape
+            xk = torch.from_numpy(xk_np).cuda()
+            if wk.is_forest:
+                model = dt.Forest(wk.nodes, wk.tree_offsets, wk.n_features, wk.n_classes)
+                want_k = oracle.forest_classes(wk.nodes, wk.tree_offsets, xk_np, Fk,
+                                               wk.n_classes, threads=threads)
+                algos_k = ["data", "speculative"]
+            else:
+                model = dt.Tree(wk.nodes, wk.n_features, wk.n_classes)
+                want_k = oracle.tree_classes(wk.nodes, xk_np, Fk, threads=threads)
+                algos_k = ["data", "speculative", "path"]
+            fbytes = nk * Fk * 4
+            entry = {"workload": W.CONFIG_DESCRIPTIONS[k], "records": nk, "n_features": Fk,
+                     "feature_bytes": fbytes, "algorithmic_bytes_per_launch": nk * (4 * Fk + 1),
+                     "decompositions": {}}
+            for algo in algos_k:
+                wall, ks, got = timed(model, xk, algo, args.steps, args.warmup, nrec=nk)
+                kc = timed_cold(model, xk, algo, args.steps, nrec=nk)
+                kavg = float(ks.mean())
+                r_k = {"kernel_us": kernel_stats(ks), "kernel_us_cold": kernel_stats(kc),
+                       "samples_per_s": nk / (wall / args.steps),
+                       "kernel_samples_per_s": nk / kavg,
+                       "hbm_gbps": nk * (4 * Fk + 1) / kavg / 1e9,
+                       "hbm_frac_of_peak": nk * (4 * Fk + 1) / kavg / 1e9 / PEAK_HBM_GBPS,
+                       "hbm_frac_of_peak_cold": nk * (4 * Fk + 1) / float(kc.mean()) / 1e9
+                                                / PEAK_HBM_GBPS,
+                       "mismatches_vs_oracle": int((got != want_k).sum())}
+                if wk.is_forest:
+                    steps_k = nk * forest_depth_sum(wk)
+                    r_k["tree_samples_per_s"] = nk * (len(wk.tree_offsets) - 1) / kavg
+                    r_k["roofline_alu"] = {"bound": "alu", "unit": "T compares/s",
+                                           "peak": PEAK_COMPARES_T,
+                                           "achieved": steps_k / kavg / 1e12,
+                                           "frac": steps_k / kavg / 1e12 / PEAK_COMPARES_T,
+                                           "compares_per_launch": steps_k}
+                else:
+                    r_k["launch"] = model.launch_info(xk, algo=algo, out_kind="class_u8")
+                entry["decompositions"][algo] = r_k
+                log("config", wk.name, algo, json.dumps(r_k))
+            configs[wk.name] = entry
+            model.close()
+            del xk
+            torch.cuda.empty_cache()
 
     narrow = None
     narrow_case = None
@@ -511,8 +597,13 @@ def main() -> int:
                           "compares_per_launch": n * forest_depth_sum(w),
                           "kernel": r["kernel"]}
                          if w.is_forest else None),
-        "parity": "bit-exact vs oracle on all %d records" % n
+        "parity": "bit-exact vs oracle on all records of every timed workload"
                   if all(v["mismatches_vs_oracle"] == 0 for v in results.values()) and
+                  (depth_sweep is None or
+                   all(v["mismatches_vs_oracle"] == 0 for v in depth_sweep.values())) and
+                  (configs is None or
+                   all(r["mismatches_vs_oracle"] == 0 for c in configs.values()
+                       for r in c["decompositions"].values())) and
                   (outer is None or
                    all(v["mismatches_vs_oracle"] == 0 for v in outer["schemes"].values())) and
                   (narrow is None or
@@ -525,6 +616,8 @@ def main() -> int:
         "path_over_speculative_kernel_time": (
             results["path"]["kernel_us"]["avg"] / results["speculative"]["kernel_us"]["avg"]
             if "path" in results and "speculative" in results else None),
+        "speculative_window_depths": depth_sweep,
+        "configs": configs,
         "narrow_records": narrow,
         "outer_time": outer,
         "paper_context": PAPER_CONTEXT,
