@@ -384,6 +384,33 @@ dt_status dt_forest_classify_host(const dt_forest *forest, dt_pipeline *pipeline
                                   const float *h_x, int64_t n, int64_t ld, void *h_out,
                                   dt_output out_kind, dt_algo algo, dt_pipeline_stats *stats);
 
+/* ---- host-resident records without allocation ----------------------------------------
+ *
+ * For callers that cannot allocate (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): dt_classify_host for fp32 records without a pipeline.
+ * The records cross to the device in chunks through a staging area that is part of the
+ * library (DT_NOALLOC_SCRATCH_BYTES bytes per device, a fixed array of the library's code
+ * object, held by each device the library runs on until the process ends); each chunk is
+ * copied in, classified and its labels copied out, one after the other on `stream`.  The
+ * call allocates no device or host memory and creates no stream or event.
+ *   h_x     host records, n rows of n_features floats, row stride ld >= n_features floats
+ *   h_out   host buffer of n uint8 or int32 labels (out_kind)
+ *   stream  a hipStream_t of the tree's device (NULL = the null stream)
+ * Synchronous: returns when h_out is complete.  Inputs of any size are processed, in chunks
+ * of up to (DT_NOALLOC_SCRATCH_BYTES - 256) / (4 n_features + label bytes) records.
+ * Every call on a device shares that device's staging area, which keeps the last call's
+ * contents: calls that overlap on one device (from several host threads, or on several
+ * streams) race and must not be made.
+ * Errors: those of dt_classify_host; DT_ERR_UNSUPPORTED for a device index above 63.
+ */
+#define DT_NOALLOC_SCRATCH_BYTES (32 << 20)
+dt_status dt_classify_host_noalloc(const dt_tree *tree, const float *h_x, int64_t n,
+                                   int64_t ld, void *h_out, dt_output out_kind, dt_algo algo,
+                                   void *stream);
+
+/* Size in bytes of the per-device staging area of dt_classify_host_noalloc. */
+int64_t dt_noalloc_scratch_bytes(void);
+
 #ifdef __cplusplus
 }
 #endif

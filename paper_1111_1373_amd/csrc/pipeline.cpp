@@ -13,10 +13,12 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <chrono>
 #include <cstdint>
 #include <cstring>
 #include <functional>
+#include <mutex>
 #include <new>
 #include <thread>
 #include <vector>
@@ -363,9 +365,104 @@ dt_status classify_host(const Obj *obj, dt_pipeline *p, const void *h_x, dt_dtyp
     return rs;
 }
 
+// ---- no-allocation variant of dt_classify_host -------------------------------------------
+// For callers that cannot allocate: the records are staged through `scratch`, a fixed
+// array of the library's code object (one copy per device, held until the process ends),
+// in chunks, one after the other on the caller's stream.
+constexpr int64_t kNoAllocScratchBytes = DT_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+// Device address of `scratch` on each device, looked up once per device (with that device
+// current) and kept: in host code `scratch` names a host-side stand-in, not device memory.
+constexpr int kMaxDevices = 64;
+std::atomic<unsigned char *> g_scratch[kMaxDevices];
+std::mutex g_scratch_mutex;
+
+dt_status scratch_on(int dev, unsigned char **out) {
+    if (dev < 0 || dev >= kMaxDevices) return set_error(DT_ERR_UNSUPPORTED, "device index >= 64");
+    unsigned char *p = g_scratch[dev].load(std::memory_order_acquire);
+    if (!p) {
+        std::lock_guard<std::mutex> lock(g_scratch_mutex);
+        p = g_scratch[dev].load(std::memory_order_relaxed);
+        if (!p) {
+            void *addr = nullptr;
+            const hipError_t e = hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch));
+            if (e != hipSuccess) return set_hip_error(e, "hipGetSymbolAddress(scratch)");
+            p = static_cast<unsigned char *>(addr);
+            g_scratch[dev].store(p, std::memory_order_release);
+        }
+    }
+    *out = p;
+    return DT_OK;
+}
+
+dt_status classify_host_noalloc(const dt_tree *tree, const float *h_x, int64_t n, int64_t ld,
+                                void *h_out, dt_output out_kind, dt_algo algo,
+                                hipStream_t stream) {
+    if (!tree) return set_error(DT_ERR_INVALID_ARG, "tree is NULL");
+    const int32_t F = dtree::features_of(tree);
+    if (n < 0) return set_error(DT_ERR_INVALID_ARG, "n must be >= 0");
+    if (ld < F) return set_error(DT_ERR_INVALID_ARG, "ld must be >= n_features");
+    if (n > kMaxRows) return set_error(DT_ERR_UNSUPPORTED, "n > 2^37");
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return set_hip_error(e, "hipGetDevice");
+    if (dev != dtree::device_of(tree))
+        return set_error(DT_ERR_INVALID_ARG, "current device differs from the tree's device");
+    unsigned char *base = nullptr;
+    dt_status rs = scratch_on(dev, &base);
+    if (rs != DT_OK) return rs;
+    // argument checks of the classify call itself (algo, out_kind, classes) on no records
+    rs = dt_classify(tree, reinterpret_cast<const float *>(base), 0, F, base, out_kind, algo,
+                     stream);
+    if (rs != DT_OK || n == 0) return rs;
+    if (!h_x || !h_out) return set_error(DT_ERR_INVALID_ARG, "null host pointer");
+    if (F > kMaxFeatures) return set_error(DT_ERR_UNSUPPORTED, "n_features > 256");
+    // chunk layout in the staging area: dense records (chunk_rows x F floats), then labels
+    const int esize = out_kind == DT_OUT_CLASS_U8 ? 1 : 4;
+    const int64_t row_bytes = int64_t(F) * 4;
+    const int64_t chunk_rows = (kNoAllocScratchBytes - 256) / (row_bytes + esize) / 64 * 64;
+    const int64_t label_off = (chunk_rows * row_bytes + 255) / 256 * 256;
+    float *d_x = reinterpret_cast<float *>(base);
+    unsigned char *d_out = base + label_off;
+    const char *hx = reinterpret_cast<const char *>(h_x);
+    unsigned char *ho = static_cast<unsigned char *>(h_out);
+    for (int64_t r0 = 0; r0 < n; r0 += chunk_rows) {
+        const int64_t rows = std::min(chunk_rows, n - r0);
+        e = hipMemcpy2DAsync(d_x, size_t(row_bytes), hx + r0 * ld * 4, size_t(ld * 4),
+                             size_t(row_bytes), size_t(rows), hipMemcpyHostToDevice, stream);
+        if (e != hipSuccess) rs = set_hip_error(e, "hipMemcpy2DAsync(records)");
+        if (rs == DT_OK) rs = dt_classify(tree, d_x, rows, F, d_out, out_kind, algo, stream);
+        if (rs == DT_OK) {
+            e = hipMemcpyAsync(ho + r0 * esize, d_out, size_t(rows * esize),
+                               hipMemcpyDeviceToHost, stream);
+            if (e != hipSuccess) rs = set_hip_error(e, "hipMemcpyAsync(labels)");
+        }
+        if (rs != DT_OK) break;
+    }
+    // synchronous: the labels are in h_out, and no copy or kernel of the call is left
+    // running, on success or error
+    e = hipStreamSynchronize(stream);
+    if (rs == DT_OK && e != hipSuccess) rs = set_hip_error(e, "hipStreamSynchronize");
+    return rs;
+}
+
 }  // namespace
 
 extern "C" {
+
+dt_status dt_classify_host_noalloc(const dt_tree *tree, const float *h_x, int64_t n, int64_t ld,
+                                   void *h_out, dt_output out_kind, dt_algo algo, void *stream) {
+    try {
+        dtree::clear_error();
+        return classify_host_noalloc(tree, h_x, n, ld, h_out, out_kind, algo,
+                                     static_cast<hipStream_t>(stream));
+    } catch (...) {
+        return set_error(DT_ERR_INVALID_ARG, "unexpected internal error");
+    }
+}
+
+int64_t dt_noalloc_scratch_bytes(void) { return kNoAllocScratchBytes; }
 
 dt_status dt_pipeline_create(int32_t n_features, const dt_pipeline_options *opt,
                              dt_pipeline **out) {

@@ -103,6 +103,9 @@ _PROTOS = {
     "dt_forest_classify_host": (ctypes.c_int, [_p, _p, _p, _i64, _i64, _p, ctypes.c_int, ctypes.c_int, _p]),
     "dt_classify_host_typed": (ctypes.c_int, [_p, _p, _p, ctypes.c_int, _i64, _i64, _p, ctypes.c_int,
                                               ctypes.c_int, _p]),
+    "dt_classify_host_noalloc": (ctypes.c_int, [_p, _p, _i64, _i64, _p, ctypes.c_int, ctypes.c_int,
+                                                _p]),
+    "dt_noalloc_scratch_bytes": (_i64, []),
 }
 for _name, (_res, _args) in _PROTOS.items():
     _f = getattr(_lib, _name)
@@ -418,6 +421,30 @@ class Pipeline:
             self.close()
         except Exception:
             pass
+
+
+def noalloc_scratch_bytes() -> int:
+    """Size in bytes of the per-device staging area of ``classify_host_noalloc``."""
+    return int(_lib.dt_noalloc_scratch_bytes())
+
+
+def classify_host_noalloc(tree, x, algo: str = "data", out_kind: str = "class_u8", out=None,
+                          stream=None):
+    """``dt_classify_host_noalloc``: labels of host-resident fp32 records (numpy or CPU
+    tensor) staged through the library's fixed per-device area; returns a numpy array
+    (or fills ``out``, a numpy array of n uint8 / int32)."""
+    ptr, n, ld, xt = _host_features_arg(x, tree.n_features, "f32")
+    dtype = np.uint8 if out_kind == "class_u8" else np.int32
+    if out is None:
+        out = np.empty(n, dtype=dtype)
+    if not isinstance(out, np.ndarray) or out.dtype != dtype or out.shape != (n,) or \
+            not out.flags.c_contiguous:
+        raise TypeError("out must be a contiguous numpy array of %d %s" % (n, np.dtype(dtype)))
+    _check(_lib.dt_classify_host_noalloc(tree._h, ptr if n else None, n, ld,
+                                         out.ctypes.data if n else None, OUT_KINDS[out_kind],
+                                         ALGOS[algo], _stream_handle(stream)),
+           "dt_classify_host_noalloc")
+    return out
 
 
 def probe_read(src, sink, waves_per_cu: int = 8, stream=None):
