@@ -166,6 +166,10 @@ dt_status dt_tree_check(const dt_node *nodes, int32_t n_nodes, int32_t n_feature
  *                   -v - 1.  A leaf met above the bottom level is recorded at the exit
  *                   reached by always going right from it.
  * Window 0 is rooted at node 0; windows are numbered in breadth-first order of their roots.
+ * Windows are rooted at tree depth 0 and at depths d0, d0 + d, d0 + 2d, ...: window 0 holds
+ * d0 <= d levels (its slots below them always go right), every other window d.  d0 is d,
+ * unless the shallower d0 = depth - d * (levels - 1), which fills the deepest level of
+ * windows instead of the first, needs fewer windows (Section 6 leaves the cut points open).
  * Call with capacity_windows = 0 (buffers may be NULL) to learn *n_windows and *levels
  * (the largest number of windows on a root-to-leaf path).  Errors as dt_tree_check, plus
  * DT_ERR_INVALID_ARG for window_depth outside 1..16 or a capacity below *n_windows with

@@ -568,21 +568,27 @@ struct Spec {
     using N = Node<XT>;
     using Slot = typename N::S;
     static constexpr int S = 1 << D;
-    // Tiles of TR records: 64, or 32 for 64-lane groups (one record per round, so a round
-    // count of TR covers the tile; lanes >= TR carry no record).
-    static_assert(TR == kTileRows || (S == 64 && TR == 32), "32-record tiles need 64-lane groups");
-    static constexpr int kRounds = S == 64 ? TR : S;
+    // Tiles of TR records: 64, or 32 for 32- and 64-lane groups.  A round evaluates one
+    // record per group, so kRounds = TR S / 64 rounds cover the tile: group s evaluates
+    // records s kRounds .. s kRounds + kRounds - 1, and record s kRounds + g lives in lane
+    // s S + g (its group's lane g).  Only 32-record tiles of 32-lane groups leave lanes
+    // without a record (g >= 16); in_record_order() moves the results to lanes 0 .. TR - 1.
+    static_assert(TR == kTileRows || (S >= 32 && TR == 32), "32-record tiles need 32- or 64-lane groups");
+    static constexpr int kRounds = TR * S / kTileRows;
     using Bits = typename std::conditional<(S > 32), uint64_t, uint32_t>::type;
     int j;          // slot evaluated by this lane (slot 0 is padding)
     int seg_shift;  // first lane of this lane's segment
+    int rec_base;   // first record of this lane's segment (segment index * kRounds)
 
-    // Record tile layout the rounds read: a 64-lane group reads one record row per round
-    // (conflict-free without the swizzle, flat rows); narrower groups read 64/S rows at
-    // once, and the swizzle keeps rows reading the same feature on distinct banks.
-    static constexpr int kLayout = S == 64 ? kRowFlat : kRowMajor;
+    // Record tile layout the rounds read.  64- and 32-lane groups read one or two record
+    // rows per round: flat rows, so that a round's row is its group's first row plus a
+    // constant (an instruction offset; a per-row swizzle would be a per-round register).
+    // Narrower groups read 64/S rows at once, and the swizzle keeps rows reading the same
+    // feature on distinct banks.
+    static constexpr int kLayout = S >= 32 ? kRowFlat : kRowMajor;
 
     __device__ __forceinline__ explicit Spec(int lane)
-        : j(lane & (S - 1)), seg_shift(lane & ~(S - 1)) {}
+        : j(lane & (S - 1)), seg_shift(lane & ~(S - 1)), rec_base((lane >> D) * kRounds) {}
 
     // Value wb of lane seg_shift + G (record seg_shift + G's window byte offset) in every
     // lane of the segment, with the round index G a compile-time constant:
@@ -646,8 +652,8 @@ struct Spec {
                              reinterpret_cast<const char *>(slots + j) + window_of<G0 + G>(wb))),
          ...);
         T xv[K];
-        ((xv[G] = feature_at<XT, 1>(tile + (seg_shift + G0 + G) * RS, p[G],
-                                    kLayout == kRowFlat ? 0 : swz_el<XT, RS>(seg_shift + G0 + G))),
+        ((xv[G] = feature_at<XT, 1>(tile + (rec_base + G0 + G) * RS, p[G],
+                                    kLayout == kRowFlat ? 0 : swz_el<XT, RS>(rec_base + G0 + G))),
          ...);
         (take<G0 + G>(bits, __ballot(N::right(xv[G], p[G]))), ...);
         __builtin_amdgcn_sched_barrier(0);
@@ -731,7 +737,7 @@ struct Spec {
         } else {
             int w = 0;
             int32_t code = exits[walk(eval(slots, true, root, 0, tile))];
-            bool done = code < 0 || (TR < kTileRows && j >= TR);   // lanes without a record
+            bool done = code < 0 || (TR < kTileRows && j >= kRounds);   // lanes without a record
             if (!done) w = code;
             for (int level = 1; level < levels; ++level) {
                 if (__all(done)) break;
@@ -743,6 +749,18 @@ struct Spec {
                 }
             }
             return code;
+        }
+    }
+
+    // Lane r's result for record r of the tile (r < TR).  With 32-record tiles of 32-lane
+    // groups, records 16..31 live in lanes 32..47: one ds_bpermute brings them down.
+    __device__ __forceinline__ int32_t in_record_order(int32_t v) const {
+        if constexpr (S == 32 && TR == 32) {
+            const int lane = seg_shift + j;
+            const int src = lane < 16 ? lane : lane + 16;   // lanes >= 32 carry no record
+            return __builtin_amdgcn_ds_bpermute((src & 63) << 2, v);
+        } else {
+            return v;
         }
     }
 };

@@ -190,18 +190,17 @@ std::vector<const void *> g_prepared;
 // add contention.  The speculative decomposition, which does 2^D times the lane work per
 // record, is bound by LDS latency once the tiles are small, and then gains from every
 // wavefront up to 16 per CU (uint8 records of 64 features: 207 us with 16 against 282 us
-// with 8); with 16 KiB tiles (64 fp32 features) 64 KiB in flight is again the better
-// point: 4 wavefronts keep a larger result buffer next to the tables and measure 640 us
-// on 16,777,216 x 64 records against 674 us with 5.  Its 64-lane groups (32-record tiles)
-// issue 64 slot evaluations per record and level and gain up to 96 KiB of tiles per CU:
-// 730 us with 12 wavefronts of 8 KiB tiles against 775 us with 8 on the same records.
+// with 8).  With tiles of 64 fp32 features 64 KiB in flight is again the better point:
+// 4 wavefronts of 16 KiB tiles keep a larger result buffer next to the tables (640 us on
+// 16,777,216 x 64 records against 674 us with 5), and so do 8 of the 8 KiB tiles of 32
+// records that depth-5 and depth-6 windows use (682 us against 726 us with 12 at depth
+// 6, 710 against 729 us at depth 5).
 // The path reduction is latency-bound and takes as many wavefronts as fit, up to 8.
-int target_waves_per_cu(int algo, int tile_bytes, int tile_rows) {
+int target_waves_per_cu(int algo, int tile_bytes) {
     const int hbm = std::max(2, std::min(32, (64 * 1024) / tile_bytes));
     if (algo == DT_ALGO_DATA) return hbm;
     if (algo == DT_ALGO_SPECULATIVE)
-        return tile_rows < dtree::kTileRows ? std::min(16, (96 * 1024) / tile_bytes)
-                                            : std::min(16, hbm);
+        return std::min(16, hbm);
     return 8;
 }
 
@@ -254,7 +253,7 @@ dt_status make_plan(const DeviceCaps &caps, int algo, int elem_type, int row_str
     if (plan->status != DT_OK) return plan->status;
 
     const int target =
-        waves_per_cu > 0 ? waves_per_cu : target_waves_per_cu(algo, record_tile_bytes, tile_rows);
+        waves_per_cu > 0 ? waves_per_cu : target_waves_per_cu(algo, record_tile_bytes);
     // Try every workgroup size and count per CU; keep the shape reaching the most resident
     // wavefronts up to the target (registers and the LDS both limit residency); on ties
     // prefer larger workgroups (fewer table copies), then a larger result buffer.
@@ -887,8 +886,8 @@ dt_status dt_tree_check(const dt_node *nodes, int32_t n_nodes, int32_t n_feature
             int dd, sd;
             window_depths(nodes, shape, n_features, opt, &dd, &sd);
             fill_info(shape, n_features, n_classes, dd, dtree::count_windows(nodes, shape, dd),
-                      dtree::count_levels(shape, dd), sd, dtree::count_windows(nodes, shape, sd),
-                      dtree::count_levels(shape, sd), info);
+                      dtree::count_levels(nodes, shape, dd), sd, dtree::count_windows(nodes, shape, sd),
+                      dtree::count_levels(nodes, shape, sd), info);
         }
         return DT_OK;
     } catch (const std::bad_alloc &) {
@@ -925,7 +924,7 @@ dt_status dt_encode_windows(const dt_node *nodes, int32_t n_nodes, int32_t n_fea
         if (nw * (int64_t(1) << window_depth) > (int64_t(1) << 30))
             return fail(DT_ERR_UNSUPPORTED, "window tables too large");
         if (n_windows) *n_windows = int32_t(nw);
-        if (levels) *levels = dtree::count_levels(shape, window_depth);
+        if (levels) *levels = dtree::count_levels(nodes, shape, window_depth);
         if (capacity_windows == 0) return DT_OK;
         if (capacity_windows < nw) return fail(DT_ERR_INVALID_ARG, "capacity_windows too small");
         if (!features || !thresholds || !exit_class || !exit_leaf)

@@ -73,18 +73,45 @@ dt_status validate_tree(const dt_node *nodes, int32_t n_nodes, int32_t n_feature
     return DT_OK;
 }
 
-int64_t count_windows(const dt_node *nodes, const TreeShape &shape, int depth) {
-    // window roots: the root and every decision node whose depth is a positive multiple
-    // of the window depth
+namespace {
+
+// Window roots for window depth D and first-window depth d0: the root and every decision
+// node at depth d0 + m D (m >= 0).
+int64_t count_roots(const dt_node *nodes, const TreeShape &shape, int depth, int first) {
     int64_t n = 1;
-    for (int32_t i = 1; i < shape.n_nodes; ++i)
-        if (nodes[i].cls == -1 && shape.node_depth[i] % depth == 0) ++n;
+    for (int32_t i = 1; i < shape.n_nodes; ++i) {
+        const int32_t d = shape.node_depth[i];
+        if (nodes[i].cls == -1 && d >= first && (d - first) % depth == 0) ++n;
+    }
     return n;
 }
 
-int32_t count_levels(const TreeShape &shape, int depth) {
-    // a leaf at depth d is reached in window level ceil(d / D) - 1
-    return std::max(1, (shape.depth + depth - 1) / depth);
+}  // namespace
+
+int first_window_depth(const dt_node *nodes, const TreeShape &shape, int depth) {
+    // The window levels a record passes through are ceil(depth_of_tree / D) either way;
+    // rooting the windows at d0, d0 + D, ... with d0 = depth_of_tree - D (levels - 1)
+    // fills the deepest level of windows instead of the first, which often needs far fewer
+    // windows (a complete depth-12 tree at D = 5: 1 + 4 + 128 against 1 + 32 + 1024).
+    if (shape.depth <= depth) return depth;
+    const int levels = (shape.depth + depth - 1) / depth;
+    const int shallow = shape.depth - depth * (levels - 1);
+    if (shallow == depth) return depth;
+    return count_roots(nodes, shape, depth, shallow) < count_roots(nodes, shape, depth, depth)
+               ? shallow
+               : depth;
+}
+
+int64_t count_windows(const dt_node *nodes, const TreeShape &shape, int depth) {
+    return count_roots(nodes, shape, depth, first_window_depth(nodes, shape, depth));
+}
+
+int32_t count_levels(const dt_node *nodes, const TreeShape &shape, int depth) {
+    // a leaf at depth d <= d0 is reached in window level 0, a deeper one in level
+    // ceil((d - d0) / D)
+    const int first = first_window_depth(nodes, shape, depth);
+    if (shape.depth <= first) return 1;
+    return 1 + (shape.depth - first + depth - 1) / depth;
 }
 
 void build_windows(const dt_node *nodes, const TreeShape &shape, int depth, WindowTables *out) {
@@ -92,7 +119,9 @@ void build_windows(const dt_node *nodes, const TreeShape &shape, int depth, Wind
     const float neg_inf = -std::numeric_limits<float>::infinity();
     out->depth = depth;
     out->slots = S;
-    out->levels = count_levels(shape, depth);
+    const int first = first_window_depth(nodes, shape, depth);
+    out->first_depth = first;
+    out->levels = count_levels(nodes, shape, depth);
     const int64_t nw = count_windows(nodes, shape, depth);
     out->n_windows = int32_t(nw);
     out->feature.assign(size_t(nw) * S, 0);
@@ -108,6 +137,9 @@ void build_windows(const dt_node *nodes, const TreeShape &shape, int depth, Wind
         std::fill(slot_node.begin(), slot_node.end(), -1);
         slot_node[0] = roots[w];
         const size_t base = w * size_t(S);
+        // decision levels of this window: d0 for window 0, D for the others; a shallower
+        // window's slots below its last level stay always-right padding
+        const int dw = w == 0 ? first : depth;
         // h is the 0-based heap index of the working array (stored at slot h + 1).
         // Unreachable exits end the walk like any leaf would; they stay -1.
         for (int32_t h = 0; h < S - 1; ++h) {
@@ -127,10 +159,12 @@ void build_windows(const dt_node *nodes, const TreeShape &shape, int depth, Wind
             for (int32_t b = 0; b < 2; ++b) {
                 const int32_t c = nodes[n].left + b;
                 const int32_t hc = 2 * h + 1 + b;
-                if (hc < S - 1) {
+                if (hc < (1 << dw) - 1) {
                     slot_node[size_t(hc)] = c;
                 } else {
-                    const int32_t e = hc - (S - 1);
+                    // child at the window's last level dw: always-right slots below it
+                    // (none when dw = D) lead to its exit
+                    const int32_t e = ((hc + 2) << (depth - dw)) - 2 - (S - 1);
                     if (nodes[c].cls != -1) {
                         out->exit_class[base + size_t(e)] = -(nodes[c].cls + 1);
                         out->exit_leaf[base + size_t(e)] = -(c + 1);
@@ -229,7 +263,7 @@ int choose_data_window_depth(const dt_node *nodes, const TreeShape &shape, int64
             smallest_bytes = bytes;
         }
         if (bytes > max_bytes) continue;
-        const int32_t levels = count_levels(shape, d);
+        const int32_t levels = count_levels(nodes, shape, d);
         if (best == 0 || levels < best_levels || (levels == best_levels && bytes < best_bytes)) {
             best = d;
             best_levels = levels;

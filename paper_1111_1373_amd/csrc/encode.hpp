@@ -45,6 +45,7 @@ struct WindowTables {
     int32_t slots = 0;        // S = 2^D
     int32_t n_windows = 0;
     int32_t levels = 0;       // windows on the longest root-to-leaf path
+    int32_t first_depth = 0;  // decision levels of window 0 (d0 <= D; the others have D)
     std::vector<int32_t> feature;
     std::vector<float> threshold;
     std::vector<int32_t> exit_class;
@@ -60,9 +61,15 @@ struct WindowTables {
 uint32_t narrow_key(float t, dt_dtype type);
 void build_narrow_slots(const WindowTables &wt, dt_dtype type, std::vector<uint32_t> *out);
 
-// Number of windows for window depth D (without building them).
+// Depth d0 of the first window for window depth D: windows are rooted at tree depth 0 and
+// at depths d0, d0 + D, d0 + 2D, ...  d0 is D, or the depth that fills the deepest level of
+// windows when that needs fewer windows.
+int first_window_depth(const dt_node *nodes, const TreeShape &shape, int depth);
+
+// Number of windows, and window levels on the longest path, for window depth D (without
+// building them).
 int64_t count_windows(const dt_node *nodes, const TreeShape &shape, int depth);
-int32_t count_levels(const TreeShape &shape, int depth);
+int32_t count_levels(const dt_node *nodes, const TreeShape &shape, int depth);
 
 void build_windows(const dt_node *nodes, const TreeShape &shape, int depth, WindowTables *out);
 

@@ -62,12 +62,13 @@ struct KArgs {
 constexpr int kPathIntsPerWave = 128;
 
 // Records per wavefront tile of a kernel: 64 (one per lane), except for the speculative
-// kernel with 64-slot windows (depth 6) on rows of at least 32 bytes in the LDS.  That
-// kernel reads one record row per round, so a tile of 32 records serves it as well while
-// taking half the LDS, and twice as many wavefronts then fit next to its window tables.
-// (Rows under 32 bytes keep 64 records: 16-byte staging needs one vector per lane.)
+// kernel with 32- and 64-slot windows (depths 5 and 6) on rows of at least 32 bytes in the
+// LDS.  That kernel reads one or two record rows per round, so a tile of 32 records serves
+// it as well while taking half the LDS, and twice as many wavefronts then fit next to its
+// window tables.  (Rows under 32 bytes keep 64 records: 16-byte staging needs one vector
+// per lane.)
 __host__ __device__ constexpr int tile_rows_for(int algo, int depth, int row_bytes) {
-    return algo == kAlgoSpec && depth == 6 && row_bytes >= 32 ? 32 : kTileRows;
+    return algo == kAlgoSpec && depth >= 5 && row_bytes >= 32 ? 32 : kTileRows;
 }
 
 // Largest workgroup of a single-tree kernel instance, in wavefronts: 8, or 16 for the

@@ -62,7 +62,7 @@ spec_kernel(KArgs a) {
     const NS root = slots[spec.j];   // window 0 is shared by every record
     const T *el = reinterpret_cast<const T *>(tile);
     dev::tile_loop<XT, RS, LOAD, Spec::kLayout, TR>(a, tile, obuf, lane, [&](int64_t) -> int32_t {
-        return ~spec.run(slots, exits, a.levels, root, el);
+        return ~spec.in_record_order(spec.run(slots, exits, a.levels, root, el));
     });
 }
 

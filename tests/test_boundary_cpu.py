@@ -286,17 +286,28 @@ def test_window_tables_reproduce_oracle(case, depth):
             assert most <= bound
 
 
-@pytest.mark.parametrize("d,D", [(4, 4), (8, 4), (12, 6), (12, 4), (12, 12), (10, 3), (5, 2)])
+@pytest.mark.parametrize("d,D", [(4, 4), (8, 4), (12, 6), (12, 4), (12, 12), (10, 3), (5, 2),
+                                 (12, 5), (11, 2), (3, 6)])
 def test_complete_tree_window_counts(d, D):
-    """Complete depth-d tree: windows are rooted at depths 0, D, 2D, ... < d, so there are
-    sum_m 2^(mD) of them, and ceil(d/D) levels."""
+    """Complete depth-d tree: a record passes ceil(d/D) window levels.  With
+    d0 = d - D (levels - 1) < D the windows are rooted at depths 0 and d0, d0 + D, ... < d:
+    window 0 holds d0 levels and every deeper window is full (fewer windows than roots at
+    0, D, 2D, ..., whose deepest windows would hold d0 levels each); with d0 = D at
+    0, D, 2D, ...  A tree no deeper than D is one window."""
     r = np.random.Generator(np.random.PCG64(d * 100 + D))
     nodes = W.complete_tree(r, d, 4, 3)
     tab = dt.encode_windows(nodes, 4, 3, D)
-    assert tab["n_windows"] == sum(1 << (m * D) for m in range(0, (d + D - 1) // D))
-    assert tab["levels"] == -(-d // D)
-    # in a complete window every slot but the padding (slot 0) holds a decision node
-    assert np.isfinite(tab["threshold"][:, 1:]).all() or d % D != 0
+    levels = -(-d // D)
+    d0 = d - D * (levels - 1)
+    roots = [0] + list(range(d0, d, D)) if d0 < D else list(range(0, d, D))
+    assert tab["n_windows"] == sum(1 << depth for depth in roots)
+    assert tab["levels"] == levels
+    # window 0: decision nodes in its first min(d0, d) heap levels, always-right padding
+    # below; every other window is complete; slot 0 is padding everywhere
+    top = min(d0, d)
+    level = np.floor(np.log2(np.arange(1, 1 << D))).astype(int)
+    np.testing.assert_array_equal(np.isfinite(tab["threshold"][0, 1:]), level < top)
+    assert np.isfinite(tab["threshold"][1:, 1:]).all()
     assert np.isneginf(tab["threshold"][:, 0]).all()
 
 
