@@ -159,6 +159,21 @@ def test_ragged_sizes(dt, n):
     _check_all_outputs(dt, t, w.nodes, x, _gpu(x), w.n_features)
 
 
+@pytest.mark.parametrize("sd", [5, 6])
+@pytest.mark.parametrize("n", [1, 15, 16, 17, 31, 33, 47, 63, 65, 1000, 4097])
+def test_ragged_sizes_32_record_tiles(dt, sd, n):
+    """Speculative windows of depth 5 and 6 (32- and 64-lane record groups, Section 3.4)
+    run on tiles of 32 records; at depth 5 records 16-31 of a tile are walked in lanes
+    32-47 and moved back to record order at the end.  Inputs whose last tile is partial
+    in either half of it, or a single record."""
+    w = W.config(2, n_samples=n)
+    x = w.features()
+    t = dt.Tree(w.nodes, w.n_features, w.n_classes, spec_window_depth=sd)
+    xd = _gpu(x)
+    assert t.launch_info(xd, algo="speculative")["tile_rows"] == 32
+    _check_all_outputs(dt, t, w.nodes, x, xd, w.n_features, algos=("speculative",))
+
+
 def test_empty_input(dt):
     w = W.config(1, n_samples=0)
     t = dt.Tree(w.nodes, w.n_features, w.n_classes)

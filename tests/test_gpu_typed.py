@@ -123,6 +123,19 @@ def test_ragged_and_empty(dt, x_type):
         _check(dt, t, nodes, xn[:n], x_type, w.n_features, outs=("class_u8",))
 
 
+@pytest.mark.parametrize("x_type", X_TYPES)
+@pytest.mark.parametrize("sd", [5, 6])
+def test_ragged_wide_windows(dt, x_type, sd):
+    """Speculative windows of depth 5 and 6 on narrow records (32-record tiles where the
+    rows take at least 32 bytes), on inputs whose last tile is partial."""
+    w = W.config(2, n_samples=4097)
+    xn = W.narrow_records(w.features(), x_type)
+    nodes = W.narrow_tree(w.nodes, x_type)
+    t = dt.Tree(nodes, w.n_features, w.n_classes, spec_window_depth=sd)
+    for n in (1, 17, 33, 65, 4097):
+        _check(dt, t, nodes, xn[:n], x_type, w.n_features, algos=("speculative",))
+
+
 def test_errors(dt):
     w = W.config(1, n_samples=64)
     t = dt.Tree(w.nodes, w.n_features, w.n_classes)
