@@ -311,6 +311,42 @@ def test_complete_tree_window_counts(d, D):
     assert np.isneginf(tab["threshold"][:, 0]).all()
 
 
+def _shape_cases():
+    r = np.random.Generator(np.random.PCG64(31337))
+    cases = [("random%d" % n, W.random_full_tree(r, n, 4, 3)) for n in (1, 2, 7, 40, 300, 1000)]
+    cases += [(g, W.sweep_tree(g, 4, 3)) for g in ("grown", "random1023", "paper15", "chain64")]
+    return cases
+
+
+@pytest.mark.parametrize("case", _shape_cases(), ids=lambda c: c[0])
+@pytest.mark.parametrize("D", [1, 2, 3, 4, 5, 6])
+def test_window_cut_choice(case, D):
+    """Where windows are cut: roots at depth 0 and at d0 + mD, with d0 = D or the shallow
+    first window d0 = depth - D (levels - 1), whichever needs fewer windows (ties: D).
+    Counted here from the nodes' depths, independently of the encoder; a record passes
+    ceil(depth / D) windows either way, and window 0 holds decision nodes in its first d0
+    heap levels only."""
+    _, nodes = case
+    d = TU.depths(nodes)
+    inner = nodes["cls"] == -1
+    td = int(d.max())
+    levels = max(1, -(-td // D))
+
+    def roots(d0):
+        return 1 + int(np.sum(inner & (d >= d0) & ((d - d0) % D == 0) & (d > 0)))
+
+    shallow = td - D * (levels - 1)
+    d0 = shallow if (td > D and shallow < D and roots(shallow) < roots(D)) else D
+    tab = dt.encode_windows(nodes, 4, 3, D)
+    assert tab["n_windows"] == roots(d0)
+    assert tab["levels"] == levels
+    # window 0 holds exactly the decision nodes above depth d0, in heap levels below d0
+    lvl = np.floor(np.log2(np.arange(1, 1 << D))).astype(int)
+    finite = np.isfinite(tab["threshold"][0, 1:])
+    assert not finite[lvl >= d0].any()
+    assert int(finite.sum()) == int(np.sum(inner & (d < d0)))
+
+
 def test_default_depths_and_info():
     w = W.config(4, n_samples=1)
     info = dt.tree_check(w.nodes, w.n_features, w.n_classes)
