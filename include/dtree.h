@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define DT_ABI_VERSION 5
+#define DT_ABI_VERSION 6
 
 typedef enum {
     DT_OK = 0,

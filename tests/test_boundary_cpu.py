@@ -42,7 +42,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version_and_strings():
-    assert dt.ABI_VERSION == 5
+    assert dt.ABI_VERSION == 6
     for s in range(6):
         assert dt._lib.dt_status_string(s)
     assert dt._lib.dt_status_string(99) == b"unknown status"
