@@ -253,7 +253,10 @@ dt_status dt_tree_launch_info(const dt_tree *tree, const void *d_x, dt_dtype x_t
  *   algo    DT_ALGO_DATA, DT_ALGO_SPECULATIVE or DT_ALGO_PATH; all give identical
  *           results
  * Exactly n outputs are written; nothing is written on an error return.  Buffers are
- * owned by the caller and must stay valid until the work on `stream` completes.
+ * owned by the caller and must stay valid until the work on `stream` completes.  The call
+ * puts one kernel launch on `stream` and nothing else (no allocation, copy, memset or
+ * synchronisation), so it may be captured in a HIP graph; a tree handle is never written
+ * after creation, so calls on several streams may use it at once.
  * Errors: DT_ERR_INVALID_ARG (null tree or pointers with n > 0, n < 0, ld < n_features,
  * unknown enum, DT_OUT_CLASS_U8 with n_classes > 256, device other than the tree's),
  * DT_ERR_UNSUPPORTED (n_features > 256, n > 2^37), DT_ERR_HIP (launch failure).
@@ -296,8 +299,8 @@ void dt_forest_destroy(dt_forest *forest);
 /*
  * Majority vote of the forest's trees for n records; ties go to the smallest class id
  * (Section 1's forests; each tree evaluated as dt_classify, Sections 3.2-3.4).
- * Arguments and errors as dt_classify; out_kind must be DT_OUT_CLASS_U8 or
- * DT_OUT_CLASS_I32.
+ * Arguments, errors, graph capture and concurrent use as dt_classify; out_kind must be
+ * DT_OUT_CLASS_U8 or DT_OUT_CLASS_I32.
  */
 dt_status dt_forest_classify(const dt_forest *forest, const float *d_x, int64_t n, int64_t ld,
                              void *d_out, dt_output out_kind, dt_algo algo, void *stream);
