@@ -1,7 +1,7 @@
 """Seeded random GPU parity cases: tree shape, feature count, classes, record type,
 layout, decomposition, window depths and output kind all drawn at random (and random
-forests of 1 to 255 trees), each case
-checked element by element against the oracle on the (widened) records."""
+forests of 1 to 255 trees), each case checked element by element against the oracle on
+the (widened) records."""
 import numpy as np
 import pytest
 
