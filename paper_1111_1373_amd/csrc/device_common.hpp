@@ -499,12 +499,17 @@ __device__ __forceinline__ void walk_data_k(const char *const (&base)[K],
     constexpr bool kPacked = std::is_same<EX, PackedExits>::value;
     int k0 = 0;
     if (D >= (kPacked ? 2 : 1)) {
+        // the K scalar loads first, then the K feature reads, then the K steps: one wait
+        // for each instead of a scalar-load and an LDS round trip per tree (the two kinds
+        // share one wait counter)
+        TopSlots top[K];
+        float xv[K];
 #pragma unroll
-        for (int i = 0; i < K; ++i) {
-            const TopSlots top = top_slots(gbase[i]);
-            const float xv = feature_at<kXF32, STRIDE>(row, top.s1, sw);
-            p[i] = heap_step(1, !(xv < top.s1.t));
-        }
+        for (int i = 0; i < K; ++i) top[i] = top_slots(gbase[i]);
+#pragma unroll
+        for (int i = 0; i < K; ++i) xv[i] = feature_at<kXF32, STRIDE>(row, top[i].s1, sw);
+#pragma unroll
+        for (int i = 0; i < K; ++i) p[i] = heap_step(1, !(xv[i] < top[i].s1.t));
         k0 = 1;
     }
     for (int level = 0; level < max_levels; ++level) {
