@@ -455,26 +455,13 @@ __device__ __forceinline__ int32_t walk_data(const typename Node<XT>::S *slots,
     return code;
 }
 
-// The root slot (slot 1) of a tree's window 0 as a wavefront-uniform value, read from the
-// tree's tables in global memory through the constant address space (one scalar load).
-struct TopSlots {
-    Slot s1;
-};
-
-__device__ __forceinline__ TopSlots top_slots(const char *window0) {
-    typedef int v4i_ __attribute__((ext_vector_type(4)));
-    typedef const __attribute__((address_space(4))) v4i_ ConstV4i_;
-    const v4i_ v = *((ConstV4i_ *)(window0));
-    return TopSlots{Slot{__int_as_float(v[2]), v[3]}};
-}
-
 // Data decomposition over K trees at once (forests): the K walks of one record are
 // independent, so interleaving them keeps K LDS dependency chains in flight per lane.
-// Tree i's tables start at base[i] (LDS or global memory) and, in global memory, at
-// gbase[i]; all trees share the window depth D.
+// Tree i's tables start at base[i] (LDS or global memory) and its window 0's root slot
+// (slot 1) is root[i], a wavefront-uniform value; all trees share the window depth D.
 template <int K, int STRIDE = 1, class EX = int32_t>
 __device__ __forceinline__ void walk_data_k(const char *const (&base)[K],
-                                            const char *const (&gbase)[K],
+                                            const Slot (&root)[K],
                                             const int (&slot_bytes)[K], const int (&levels)[K],
                                             int D, const float *row, int sw, int32_t (&code)[K]) {
     // K independent chains already hide the LDS latency, so each level reads just the
@@ -499,17 +486,12 @@ __device__ __forceinline__ void walk_data_k(const char *const (&base)[K],
     constexpr bool kPacked = std::is_same<EX, PackedExits>::value;
     int k0 = 0;
     if (D >= (kPacked ? 2 : 1)) {
-        // the K scalar loads first, then the K feature reads, then the K steps: one wait
-        // for each instead of a scalar-load and an LDS round trip per tree (the two kinds
-        // share one wait counter)
-        TopSlots top[K];
+        // the K feature reads first, then the K steps: one wait for all of them
         float xv[K];
 #pragma unroll
-        for (int i = 0; i < K; ++i) top[i] = top_slots(gbase[i]);
+        for (int i = 0; i < K; ++i) xv[i] = feature_at<kXF32, STRIDE>(row, root[i], sw);
 #pragma unroll
-        for (int i = 0; i < K; ++i) xv[i] = feature_at<kXF32, STRIDE>(row, top[i].s1, sw);
-#pragma unroll
-        for (int i = 0; i < K; ++i) p[i] = heap_step(1, !(xv[i] < top[i].s1.t));
+        for (int i = 0; i < K; ++i) p[i] = heap_step(1, !(xv[i] < root[i].t));
         k0 = 1;
     }
     for (int level = 0; level < max_levels; ++level) {

@@ -326,7 +326,9 @@ struct ForestEncoding {
     int32_t depth = 0;
     void *d_mem = nullptr;
     const int4 *d_tables = nullptr, *d_trees = nullptr, *d_chunks = nullptr;
+    const int2 *d_roots = nullptr;
     std::vector<int4> trees;     // host copy of the descriptors
+    std::vector<int2> roots;     // per tree: slot 1 of window 0 {threshold bits, feature bytes}
     std::vector<int4> chunks;    // host copy of the chunks
     int64_t table_bytes = 0;
     int64_t max_tree_bytes = 0;
@@ -519,6 +521,7 @@ void encode_forest(const dt_node *nodes, const int32_t *offsets, int32_t n_trees
                    std::vector<unsigned char> *bytes, ForestEncoding *enc) {
     enc->depth = depth;
     enc->trees.assign(size_t(n_trees), int4{0, 0, 0, 0});
+    enc->roots.assign(size_t(n_trees), int2{0, 0});
     enc->max_tree_bytes = 0;
     bytes->clear();
     std::vector<dtree::WindowTables> wts(static_cast<size_t>(n_trees));
@@ -569,6 +572,9 @@ void encode_forest(const dt_node *nodes, const int32_t *offsets, int32_t n_trees
             std::memcpy(p + sb, wt.exit_class.data(), size_t(n_slots * 4));
         }
         enc->trees[size_t(k)] = int4{int(off), int(sb), wt.levels, 0};
+        int2 root{0, 0};                          // the slot just written for slot 1
+        std::memcpy(&root, p + 8, 8);
+        enc->roots[size_t(k)] = root;
         enc->max_tree_bytes = std::max(enc->max_tree_bytes, sb + eb);
     }
     enc->table_bytes = int64_t(bytes->size());
@@ -637,10 +643,12 @@ dt_status upload_forest(const std::vector<unsigned char> &bytes, ForestEncoding 
     const int64_t tb = align16(int64_t(bytes.size()));
     const int64_t db = int64_t(enc->trees.size()) * 16;
     const int64_t cb = int64_t(enc->chunks.size()) * 16;
-    std::vector<unsigned char> host(size_t(tb + db + cb), 0);
+    const int64_t rb = int64_t(enc->roots.size()) * 8;
+    std::vector<unsigned char> host(size_t(tb + db + cb + rb), 0);
     std::memcpy(host.data(), bytes.data(), bytes.size());
     std::memcpy(host.data() + tb, enc->trees.data(), size_t(db));
     std::memcpy(host.data() + tb + db, enc->chunks.data(), size_t(cb));
+    std::memcpy(host.data() + tb + db + cb, enc->roots.data(), size_t(rb));
     hipError_t e = hipMalloc(&enc->d_mem, host.size());
     if (e != hipSuccess) {
         enc->d_mem = nullptr;
@@ -652,6 +660,7 @@ dt_status upload_forest(const std::vector<unsigned char> &bytes, ForestEncoding 
     enc->d_tables = reinterpret_cast<const int4 *>(base);
     enc->d_trees = reinterpret_cast<const int4 *>(base + tb);
     enc->d_chunks = reinterpret_cast<const int4 *>(base + tb + db);
+    enc->d_roots = reinterpret_cast<const int2 *>(base + tb + db + cb);
     return DT_OK;
 }
 
@@ -823,6 +832,7 @@ dt_status forest_classify_impl(const dt_forest *f, const float *d_x, int64_t n, 
     a.in = make_rows(d_x, dtree::kXF32, n, ld, f->n_features);
     a.tables = enc.d_tables;
     a.trees = enc.d_trees;
+    a.roots = enc.d_roots;
     a.chunks = enc.d_chunks;
     a.n_trees = f->n_trees;
     a.n_chunks = int32_t(enc.chunks.size());

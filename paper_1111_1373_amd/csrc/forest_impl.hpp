@@ -33,6 +33,16 @@ __device__ __forceinline__ int4 read_const(const int4 *p, int i) {
     return int4{v.x, v.y, v.z, v.w};
 }
 
+typedef int v2i __attribute__((ext_vector_type(2)));
+typedef const __attribute__((address_space(4))) v2i ConstV2i;
+
+// Root slot of tree i's window 0 (from the per-tree root array): a scalar load that does
+// not wait for the tree's descriptor.
+__device__ __forceinline__ Slot read_root(const int2 *p, int i) {
+    const v2i v = ((ConstV2i *)(p))[i];
+    return Slot{__int_as_float(v.x), v.y};
+}
+
 template <int NV>
 __device__ __forceinline__ void add_vote(uint32_t (&votes)[NV], int cls) {
     if constexpr (NV == 2) {
@@ -210,18 +220,27 @@ __global__ void __launch_bounds__(64 * forest_max_waves(SD == 0 ? 0 : 1, SD, RS)
                 // K trees of the chunk walked together from tree k0
                 auto walk_group = [&](auto kk, int k0) {
                     constexpr int K = decltype(kk)::value;
-                    const char *base[K], *gb[K];
+                    const char *base[K];
+                    Slot root[K];
                     int sb[K], lv[K];
                     int32_t code[K];
 #pragma unroll
                     for (int i = 0; i < K; ++i) {
                         const int4 d = read_const(a.trees, k0 + i);   // {byte_off, slot_bytes, levels, 0}
+                        root[i] = read_root(a.roots, k0 + i);
                         base[i] = cbase + (d.x - cofs);
-                        gb[i] = reinterpret_cast<const char *>(a.tables) + d.x;
                         sb[i] = d.y;
                         lv[i] = d.z;
                     }
-                    dev::walk_data_k<K, kStride, EX>(base, gb, sb, lv, a.depth, row, sw, code);
+                    // Both kinds of scalar loads complete here, before the walk: one wait
+                    // for them all, instead of one for the roots and, after the root step,
+                    // another for the descriptors (which the compiler would otherwise sink
+                    // to their first use).
+#pragma unroll
+                    for (int i = 0; i < K; ++i)
+                        asm volatile("" ::"s"(base[i]), "s"(sb[i]), "s"(lv[i]), "s"(root[i].t),
+                                     "s"(root[i].f));
+                    dev::walk_data_k<K, kStride, EX>(base, root, sb, lv, a.depth, row, sw, code);
 #pragma unroll
                     for (int i = 0; i < K; ++i) add_vote(votes, ~code[i]);
                 };

@@ -92,6 +92,7 @@ struct FArgs {
     Rows in;
     const int4 *tables;
     const int4 *trees;
+    const int2 *roots;       // per tree: the root slot {threshold bits, feature byte offset}
     const int4 *chunks;
     int32_t n_trees;
     int32_t n_chunks;
