@@ -425,20 +425,25 @@ __device__ __forceinline__ int heap_step(int p, bool b) {
 // `row[(f ^ sw) * STRIDE]` is feature f of this lane's record: STRIDE 1 for row-major
 // tiles, kTileRows (and sw = 0) for column-major ones.  Exit codes are EX: int32, or int16
 // where a forest's codes all fit (sign-extended when read).
+// `root0` is slot 1 of window 0, the same for every record (read once by the caller).
+// The bottom step reads the exits of both children of its node together with the node's
+// feature, and the comparison picks one: no exit read after the last comparison.
 template <int XT, int STRIDE = 1, class EX = int32_t>
 __device__ __forceinline__ int32_t walk_data(const typename Node<XT>::S *slots,
                                              const EX *exits, int D, int levels,
-                                             const typename Elem<XT>::T *row, int sw) {
+                                             const typename Elem<XT>::T *row, int sw,
+                                             const typename Node<XT>::S &root0) {
     using N = Node<XT>;
     using NS = typename N::S;
     using Pair = typename N::Pair;
+    struct alignas(2 * sizeof(EX)) ExitPair { EX l, r; };
     const int S = 1 << D;
     int w = 0;
     int32_t code = -1;
     for (int level = 0; level < levels; ++level) {
         const NS *win = slots + (w << D);
         int p = 1;
-        NS s = win[1];
+        NS s = level == 0 ? root0 : win[1];
         for (int k = 1; k < D; ++k) {
             const auto xv = feature_at<XT, STRIDE>(row, s, sw);
             const Pair kids = *reinterpret_cast<const Pair *>(win + 2 * p);
@@ -446,9 +451,11 @@ __device__ __forceinline__ int32_t walk_data(const typename Node<XT>::S *slots,
             p = heap_step(p, right);
             s = right ? kids.r : kids.l;
         }
+        // exits of children 2p and 2p + 1 of the bottom node p: an aligned pair (2p - S is
+        // even)
+        const ExitPair e = *reinterpret_cast<const ExitPair *>(exits + (w << D) + 2 * p - S);
         const auto xv = feature_at<XT, STRIDE>(row, s, sw);
-        p = heap_step(p, N::right(xv, s));
-        code = int32_t(exits[(w << D) + p - S]);
+        code = int32_t(N::right(xv, s) ? e.r : e.l);
         if (code < 0) break;
         w = code;
     }

@@ -38,8 +38,9 @@ __global__ void __launch_bounds__(512) data_kernel(KArgs a) {
     dev::wave_buffers<XT, RS>(a, tiles, tile, obuf);
     const T *row = reinterpret_cast<const T *>(tile) + lane * RS;
     const int sw = dev::swz_el<XT, RS>(lane);
+    const typename dev::Node<XT>::S root0 = slots[1];   // window 0's root, for every record
     dev::tile_loop<XT, RS, LOAD>(a, tile, obuf, lane, [&](int64_t) -> int32_t {
-        return ~dev::walk_data<XT>(slots, exits, a.depth, a.levels, row, sw);
+        return ~dev::walk_data<XT>(slots, exits, a.depth, a.levels, row, sw, root0);
     });
 }
 
